@@ -1,0 +1,198 @@
+/*
+ * ebd.h -- C ABI of the MI355X (gfx950) eviction-by-design (EBD) library, libebd.so.
+ *
+ * Method: "Error Certificates for KV-Cache Eviction via Randomized Design".
+ * A "unit" is one KV-head cache (one layer, one batch row, one KV head), the
+ * object of Sec. 3.1.  Each unit is sampled independently: a certainty set
+ * (protected positions plus tokens whose eq. (2) allocation clips at 1) is
+ * always kept and the tail is Poisson-sampled at the stored probabilities pi.
+ * Decode attention then runs over the retained rows with the Hajek weights of
+ * eq. (3) and, in the same pass, produces the Theorem 2 variance estimate and
+ * the eq. (4) radius for every query head.
+ *
+ * Conventions for every entry point:
+ *   - All data pointers are DEVICE pointers owned by the caller.  The library
+ *     allocates nothing and frees nothing; scratch space is the caller's
+ *     `workspace` buffer, sized by ebd_workspace_size().
+ *   - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
+ *   - Rows are head_dim contiguous elements; head_dim must be 128.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream).  Host-detectable argument errors are returned synchronously and
+ *     nothing is launched.  Data-dependent conditions are reported per unit
+ *     in the `status` words (EBD_ST_*), written by the kernels.
+ *   - Calls on different streams may run concurrently if they do not share
+ *     output or workspace buffers.
+ */
+#ifndef EBD_H
+#define EBD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum ebd_status {
+    EBD_OK = 0,
+    EBD_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, bad parameter */
+    EBD_ERR_UNSUPPORTED = 2, /* head_dim != 128, or no gfx950 device current */
+    EBD_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than ebd_workspace_size() */
+    EBD_ERR_HIP = 4          /* a HIP runtime call failed (launch, event) */
+} ebd_status;
+
+/* Per-unit status bits written by ebd_evict (status[u]) and ebd_append_certain. */
+#define EBD_ST_CAP_OVERFLOW 1u /* retained count exceeds the unit's capacity: rows at or
+                                  beyond the capacity are NOT written; count[u] holds the
+                                  true count; re-run with a larger capacity */
+#define EBD_ST_BUDGET_FLOOR 2u /* m <= pi_min * |T|: every tail pi equals pi_min, so the
+                                  expected size exceeds the budget */
+#define EBD_ST_NO_EVICTION 4u  /* the budget covers every positive-score tail token: all
+                                  of them get pi = 1 (zero scores keep pi_min) */
+#define EBD_ST_BAD_SCORE 8u    /* a NaN, infinite or negative score was seen; it is
+                                  treated as 0 (pi = pi_min) */
+#define EBD_ST_BAD_LAYOUT 16u  /* the unit has more rows than params.max_rows: nothing was
+                                  sampled or written for it and count[u] = 0 */
+
+/*
+ * Sampler parameters (Sec. 3.3, eq. (2) and the certainty set).
+ *   seq_off  [U+1] device int64: unit u owns full-cache rows seq_off[u] .. seq_off[u+1]-1
+ *            of `scores`, `K`, `V` (non-decreasing; uniform caches: u * n).
+ *   cap_off  [U+1] device int64: unit u owns compacted rows cap_off[u] .. cap_off[u+1]-1
+ *            of Kc, Vc, pic, idxc (its capacity).
+ *   max_rows host value >= max_u (seq_off[u+1] - seq_off[u]); sizes the launch grid.
+ *   n_sink, n_recent: protected positions i < n_sink and i >= n - n_recent (pi = 1).
+ *   budget_frac f: expected resident tokens per unit = f * n, protected ones included,
+ *            so the tail budget is m = f n - |P| (real valued).
+ *   budget_per_unit [U] device float or NULL: per-unit f overriding budget_frac.
+ *   pi_min   eps > 0, the floor of eq. (2).
+ *   pi_mode  0: lambda solves sum_T clip(lambda s_i, eps, 1) = m (expected tail size = m);
+ *            1: lambda = m / sum_T s_i, eq. (2) taken verbatim (then clipped).
+ *   seed, seed_per_unit [U] (device or NULL), epoch: the Philox4x32-10 stream.  Token i of
+ *            unit u is kept iff x < pi_i * 2^32, x = word (i mod 4) of
+ *            Philox4x32-10(counter = (i/4, u, epoch, 0x45424431), key = (seed lo, seed hi)).
+ */
+typedef struct ebd_evict_params {
+    int32_t num_units;
+    int32_t head_dim;
+    int64_t max_rows;
+    const int64_t *seq_off;
+    const int64_t *cap_off;
+    int32_t n_sink;
+    int32_t n_recent;
+    float budget_frac;
+    const float *budget_per_unit;
+    float pi_min;
+    int32_t pi_mode;
+    uint64_t seed;
+    const uint64_t *seed_per_unit;
+    uint32_t epoch;
+} ebd_evict_params;
+
+/*
+ * ebd_evict -- the Poisson tail sampler for U units (Sec. 3.3; Sec. 3.1 for deletion).
+ *   scores [rows] fp32 importance (input of eq. (2)); K, V [rows, 128] bf16.
+ *   Outputs (compacted, stable: ascending original position):
+ *     Kc, Vc [cap rows, 128] bf16   retained rows
+ *     pic    [cap rows] fp32        stored inclusion probability of each retained row
+ *     idxc   [cap rows] int32       original position (within its unit) of each row
+ *     count  [U] int32              retained rows per unit (true count, even on overflow)
+ *     lambda_out [U] fp32 or NULL   the solved scale (+inf when nothing is evicted)
+ *     pi_full [rows] fp32 or NULL   pi of every full-cache position
+ *     status [U] uint32             EBD_ST_* bits
+ *   workspace: at least ebd_workspace_size(EBD_WS_EVICT, p) bytes, 256-byte aligned.
+ *   Rows of Kc/Vc/pic/idxc beyond count[u] are left untouched.
+ */
+ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint16_t *K,
+                     const uint16_t *V, uint16_t *Kc, uint16_t *Vc, float *pic, int32_t *idxc,
+                     int32_t *count, float *lambda_out, float *pi_full, uint32_t *status,
+                     void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Certified decode attention parameters (Sec. 3.3 eq. (3), Theorem 2; Sec. 3.4 eq. (4)).
+ *   group G: query heads per KV head (q is [U, G, 128]); any G >= 1.
+ *   cap_off [U+1] device int64: the compacted layout written by ebd_evict.
+ *   max_rows host value >= max_u (cap_off[u+1] - cap_off[u]); sizes the split grid.
+ *   scale: logit scale (0 means 1/sqrt(head_dim)); delta (0 means 0.1) and eps0
+ *   (0 means 1e-9): the confidence level and normaliser of eq. (4).
+ *   split_rows: retained rows per work-group split (0 = library choice; else a multiple
+ *   of 64 in [64, 65536]).  Retained rows of a unit beyond max_rows are ignored.
+ *   flags: reserved, must be 0.
+ */
+typedef struct ebd_attend_params {
+    int32_t num_units;
+    int32_t group;
+    int32_t head_dim;
+    int32_t split_rows;
+    int64_t max_rows;
+    const int64_t *cap_off;
+    float scale;
+    float delta;
+    float eps0;
+    uint32_t flags;
+} ebd_attend_params;
+
+/*
+ * ebd_attend_certify -- one decode step of certified attention over the retained rows.
+ *   q [U, G, 128] bf16; Kc, Vc, pic, count as written by ebd_evict (rows beyond
+ *   min(count[u], capacity) are ignored).
+ *   Outputs per (unit, query head), fp32:
+ *     y      [U, G, 128]  Hajek output yhat = sum_S (a/pi) v / sum_S (a/pi)      (eq. (3))
+ *     vhat   [U, G]       variance estimate of Theorem 2
+ *     lse    [U, G]       ln Nhat, Nhat = sum_S a/pi (a = exp(scale q.k)); -inf if S empty
+ *     brange [U, G]       range term b of eq. (4) (exact maximum), or NULL
+ *     radius [U, G]       radius r of eq. (4), or NULL
+ *   workspace: at least ebd_workspace_size(EBD_WS_ATTEND, p) bytes, 256-byte aligned.
+ */
+ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
+                              const uint16_t *Vc, const float *pic, const int32_t *count,
+                              float *y, float *vhat, float *lse, float *brange, float *radius,
+                              void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * ebd_append_certain -- append one decode token per unit to its retained set with pi = 1
+ * (a recency-certainty token; the sampled draw is reused across steps, App. A.2).
+ *   k_new, v_new [U, 128] bf16; pos_new [U] int32 original positions or NULL (idx = -1).
+ *   The row goes to slot count[u] of unit u and count[u] is incremented; if the unit is
+ *   full, nothing is written, count is unchanged and EBD_ST_CAP_OVERFLOW is set in
+ *   status[u] (status may be NULL).
+ */
+ebd_status ebd_append_certain(int32_t num_units, int32_t head_dim, const int64_t *cap_off,
+                              int32_t *count, const uint16_t *k_new, const uint16_t *v_new,
+                              const int32_t *pos_new, uint16_t *Kc, uint16_t *Vc, float *pic,
+                              int32_t *idxc, uint32_t *status, void *stream);
+
+/* which-values for ebd_workspace_size */
+#define EBD_WS_EVICT 0
+#define EBD_WS_ATTEND 1
+
+/*
+ * Workspace bytes needed by ebd_evict (which = EBD_WS_EVICT, params = ebd_evict_params*)
+ * or ebd_attend_certify (EBD_WS_ATTEND, ebd_attend_params*).  Depends only on the host
+ * fields of the params (num_units, max_rows, group, split_rows).  Returns 0 on invalid
+ * arguments.
+ */
+size_t ebd_workspace_size(int32_t which, const void *params);
+
+/* Static description of a status code; never NULL. */
+const char *ebd_status_string(ebd_status s);
+
+/* Library version string, e.g. "ebd-gfx950 0.1.0". */
+const char *ebd_version(void);
+
+/*
+ * Kernel timing (profiling aid).  While enabled, every kernel launch of the library is
+ * bracketed by HIP events recorded on the launch stream.  ebd_timing_read() waits for the
+ * recorded events, and adds the elapsed times of kernel `name` ("evict_solve",
+ * "evict_compact", "attend_split", "attend_finalize", "append_certain") to *total_ms and
+ * its launch count to *launches; it then clears that kernel's record.  Not meant for use
+ * from several host threads at once.
+ */
+ebd_status ebd_timing_enable(int32_t enable);
+ebd_status ebd_timing_read(const char *name, double *total_ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EBD_H */

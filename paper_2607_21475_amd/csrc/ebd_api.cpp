@@ -1,0 +1,340 @@
+// ebd_api.cpp -- the C ABI of libebd: argument validation, workspace layout, launch planning and
+// optional per-kernel timing.  Every step of the path runs in the HIP kernels; this file only
+// checks arguments and launches them.
+#include "ebd.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "ebd_internal.hpp"
+
+namespace {
+
+using namespace ebd;
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// The library runs on gfx950 only.  Checked once per device.
+ebd_status check_device() {
+  static std::mutex mu;
+  static std::map<int, bool> ok;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return EBD_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = ok.find(dev);
+  if (it == ok.end()) {
+    hipDeviceProp_t prop;
+    bool good = false;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess)
+      good = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    it = ok.emplace(dev, good).first;
+  }
+  return it->second ? EBD_OK : EBD_ERR_UNSUPPORTED;
+}
+
+// ---- optional kernel timing ----------------------------------------------------------------
+struct TimingRec {
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
+  std::vector<hipEvent_t> pool;
+  double ms = 0.0;
+  int64_t launches = 0;
+};
+std::mutex g_tmu;
+bool g_timing = false;
+std::map<std::string, TimingRec> g_trec;
+
+hipEvent_t pooled_event(TimingRec &r) {
+  if (!r.pool.empty()) {
+    hipEvent_t e = r.pool.back();
+    r.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+hipError_t timed(const char *name, hipStream_t s, F &&launch) {
+  if (!g_timing) return launch();
+  std::lock_guard<std::mutex> lk(g_tmu);
+  TimingRec &r = g_trec[name];
+  hipEvent_t a = pooled_event(r), b = pooled_event(r);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, s);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, s);
+  if (e != hipSuccess) return e;
+  r.pending.emplace_back(a, b);
+  return hipSuccess;
+}
+
+int32_t evict_chunks(int64_t max_rows) {
+  return (int32_t)((max_rows + kEvictChunk - 1) / kEvictChunk);
+}
+
+int32_t evict_reg_chunks(int32_t nchunk) {
+  if (nchunk <= 1) return 1;
+  if (nchunk <= 2) return 2;
+  if (nchunk <= 4) return 4;
+  if (nchunk <= kEvictRegChunks) return 8;
+  return 0;
+}
+
+// Rows per split: at most 1024, halved (down to 256) until the grid has >= 2048 work-groups
+// (eight per compute unit), unless the caller fixes it.
+int32_t attend_split_rows(const ebd_attend_params *p) {
+  if (p->split_rows > 0) return p->split_rows;
+  int32_t sr = 1024;
+  while (sr > 256) {
+    const int64_t ns = (p->max_rows + sr - 1) / sr;
+    if ((int64_t)p->num_units * (ns > 0 ? ns : 1) >= 2048) break;
+    sr /= 2;
+  }
+  return sr;
+}
+
+int32_t attend_nsplit(const ebd_attend_params *p, int32_t sr) {
+  const int64_t ns = (p->max_rows + sr - 1) / sr;
+  return (int32_t)(ns > 0 ? ns : 1);
+}
+
+bool valid_evict_params(const ebd_evict_params *p) {
+  if (!p) return false;
+  if (p->num_units < 0 || p->max_rows < 0 || p->max_rows > ((int64_t)1 << 31)) return false;
+  if (p->num_units > 0 && (!p->seq_off || !p->cap_off)) return false;
+  if (p->n_sink < 0 || p->n_recent < 0) return false;
+  if (!(p->pi_min > 0.0f && p->pi_min <= 1.0f)) return false;
+  if (p->pi_mode != 0 && p->pi_mode != 1) return false;
+  if (!p->budget_per_unit && !std::isfinite(p->budget_frac)) return false;
+  return true;
+}
+
+bool valid_attend_params(const ebd_attend_params *p) {
+  if (!p) return false;
+  if (p->num_units < 0 || p->group < 1 || p->max_rows < 0 || p->max_rows > ((int64_t)1 << 31))
+    return false;
+  if (p->num_units > 0 && !p->cap_off) return false;
+  if (p->split_rows != 0 && (p->split_rows < 64 || p->split_rows > 65536 || p->split_rows % 64))
+    return false;
+  if (p->flags != 0u) return false;
+  if (p->scale < 0.0f || !std::isfinite(p->scale)) return false;
+  if (p->delta < 0.0f || p->delta >= 1.0f) return false;
+  if (p->eps0 < 0.0f || !std::isfinite(p->eps0)) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ebd_version(void) { return "ebd-gfx950 0.1.0"; }
+
+const char *ebd_status_string(ebd_status s) {
+  switch (s) {
+    case EBD_OK: return "ok";
+    case EBD_ERR_INVALID_ARG: return "invalid argument";
+    case EBD_ERR_UNSUPPORTED: return "unsupported (head_dim must be 128; device must be gfx950)";
+    case EBD_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case EBD_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+size_t ebd_workspace_size(int32_t which, const void *params) {
+  if (which == EBD_WS_EVICT) {
+    const ebd_evict_params *p = static_cast<const ebd_evict_params *>(params);
+    if (!valid_evict_params(p)) return 0;
+    return evict_workspace_bytes(p->num_units, evict_chunks(p->max_rows));
+  }
+  if (which == EBD_WS_ATTEND) {
+    const ebd_attend_params *p = static_cast<const ebd_attend_params *>(params);
+    if (!valid_attend_params(p)) return 0;
+    const int32_t sr = attend_split_rows(p);
+    return attend_workspace_bytes(p->num_units, attend_nsplit(p, sr), p->group);
+  }
+  return 0;
+}
+
+ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint16_t *K,
+                     const uint16_t *V, uint16_t *Kc, uint16_t *Vc, float *pic, int32_t *idxc,
+                     int32_t *count, float *lambda_out, float *pi_full, uint32_t *status,
+                     void *workspace, size_t ws_bytes, void *stream) {
+  if (!valid_evict_params(p)) return EBD_ERR_INVALID_ARG;
+  if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  if (p->num_units == 0) return EBD_OK;
+  if (!scores || !K || !V || !Kc || !Vc || !pic || !idxc || !count || !status)
+    return EBD_ERR_INVALID_ARG;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) ||
+      !aligned(scores, 4) || !aligned(pic, 4) || !aligned(idxc, 4))
+    return EBD_ERR_INVALID_ARG;
+  const int32_t nchunk = evict_chunks(p->max_rows);
+  const size_t need = evict_workspace_bytes(p->num_units, nchunk);
+  if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
+  const ebd_status ds = check_device();
+  if (ds != EBD_OK) return ds;
+
+  EvictLaunch L;
+  L.U = p->num_units;
+  L.nchunk = nchunk > 0 ? nchunk : 1;
+  L.reg_chunks = evict_reg_chunks(nchunk);
+  L.seq_off = p->seq_off;
+  L.cap_off = p->cap_off;
+  L.n_sink = p->n_sink;
+  L.n_recent = p->n_recent;
+  L.budget_frac = p->budget_frac;
+  L.budget_per_unit = p->budget_per_unit;
+  L.pi_min = p->pi_min;
+  L.pi_mode = p->pi_mode;
+  L.seed = p->seed;
+  L.seed_per_unit = p->seed_per_unit;
+  L.epoch = p->epoch;
+  L.scores = scores;
+  L.K = K;
+  L.V = V;
+  L.Kc = Kc;
+  L.Vc = Vc;
+  L.pic = pic;
+  L.idxc = idxc;
+  L.count = count;
+  L.lambda_out = lambda_out;
+  L.pi_full = pi_full;
+  L.status = status;
+  char *ws = static_cast<char *>(workspace);
+  L.ws_lambda = reinterpret_cast<float *>(ws);
+  L.ws_chunk_off = reinterpret_cast<int32_t *>(ws + (((size_t)L.U * sizeof(float) + 255) & ~(size_t)255));
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (timed("evict_solve", s, [&] { return launch_evict_solve(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  if (p->max_rows > 0 &&
+      timed("evict_compact", s, [&] { return launch_evict_compact(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  return EBD_OK;
+}
+
+ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
+                              const uint16_t *Vc, const float *pic, const int32_t *count,
+                              float *y, float *vhat, float *lse, float *brange, float *radius,
+                              void *workspace, size_t ws_bytes, void *stream) {
+  if (!valid_attend_params(p)) return EBD_ERR_INVALID_ARG;
+  if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  if (p->num_units == 0) return EBD_OK;
+  if (!q || !Kc || !Vc || !pic || !count || !y || !vhat || !lse) return EBD_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(pic, 4) ||
+      !aligned(y, 4))
+    return EBD_ERR_INVALID_ARG;
+  const int32_t sr = attend_split_rows(p);
+  const int32_t nsplit = attend_nsplit(p, sr);
+  const size_t need = attend_workspace_bytes(p->num_units, nsplit, p->group);
+  if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
+  const ebd_status ds = check_device();
+  if (ds != EBD_OK) return ds;
+
+  AttendLaunch L;
+  L.U = p->num_units;
+  L.G = p->group;
+  L.nsplit = nsplit;
+  L.split_rows = sr;
+  L.nhb = (p->group + kHeadBlock - 1) / kHeadBlock;
+  L.cap_off = p->cap_off;
+  L.count = count;
+  L.q = q;
+  L.Kc = Kc;
+  L.Vc = Vc;
+  L.pic = pic;
+  L.scale = p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)kHeadDim);
+  L.delta = p->delta > 0.0f ? p->delta : 0.1f;
+  L.eps0 = p->eps0 > 0.0f ? p->eps0 : 1e-9f;
+  char *ws = static_cast<char *>(workspace);
+  L.diag = reinterpret_cast<uint32_t *>(ws);
+  L.part = reinterpret_cast<float *>(ws + 256);
+  L.y = y;
+  L.vhat = vhat;
+  L.lse = lse;
+  L.brange = brange;
+  L.radius = radius;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (timed("attend_split", s, [&] { return launch_attend_split(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  if (timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  return EBD_OK;
+}
+
+ebd_status ebd_append_certain(int32_t num_units, int32_t head_dim, const int64_t *cap_off,
+                              int32_t *count, const uint16_t *k_new, const uint16_t *v_new,
+                              const int32_t *pos_new, uint16_t *Kc, uint16_t *Vc, float *pic,
+                              int32_t *idxc, uint32_t *status, void *stream) {
+  if (num_units < 0) return EBD_ERR_INVALID_ARG;
+  if (head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  if (num_units == 0) return EBD_OK;
+  if (!cap_off || !count || !k_new || !v_new || !Kc || !Vc || !pic) return EBD_ERR_INVALID_ARG;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(Kc, 16) || !aligned(Vc, 16))
+    return EBD_ERR_INVALID_ARG;
+  const ebd_status ds = check_device();
+  if (ds != EBD_OK) return ds;
+  AppendLaunch L;
+  L.U = num_units;
+  L.cap_off = cap_off;
+  L.count = count;
+  L.k_new = k_new;
+  L.v_new = v_new;
+  L.pos_new = pos_new;
+  L.Kc = Kc;
+  L.Vc = Vc;
+  L.pic = pic;
+  L.idxc = idxc;
+  L.status = status;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (timed("append_certain", s, [&] { return launch_append_certain(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  return EBD_OK;
+}
+
+ebd_status ebd_timing_enable(int32_t enable) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = enable != 0;
+  return EBD_OK;
+}
+
+ebd_status ebd_timing_read(const char *name, double *total_ms, int64_t *launches) {
+  if (!name || !total_ms || !launches) return EBD_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  auto it = g_trec.find(name);
+  *total_ms = 0.0;
+  *launches = 0;
+  if (it == g_trec.end()) return EBD_OK;
+  TimingRec &r = it->second;
+  ebd_status st = EBD_OK;
+  for (auto &ev : r.pending) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(ev.second) != hipSuccess ||
+        hipEventElapsedTime(&ms, ev.first, ev.second) != hipSuccess) {
+      st = EBD_ERR_HIP;
+    } else {
+      r.ms += ms;
+      r.launches += 1;
+    }
+    r.pool.push_back(ev.first);
+    r.pool.push_back(ev.second);
+  }
+  r.pending.clear();
+  *total_ms = r.ms;
+  *launches = r.launches;
+  r.ms = 0.0;
+  r.launches = 0;
+  return st;
+}
+
+}  // extern "C"

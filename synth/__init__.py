@@ -174,18 +174,6 @@ def make_workload_inputs(wl: Workload, units: Optional[int] = None, seed: int = 
     return {"K": K, "V": V, "seq_off": seq_off, "scores": scores, "q": q}
 
 
-def capacity(n: int, budget_frac: float, n_prot: int, extra: int = 0, align: int = 16) -> int:
-    """Rows to reserve for a unit's retained set: expected size plus 8 sd plus slack.
-
-    The retained count is |P| + a sum of independent Bernoullis with mean m and
-    variance at most m, so 8 sqrt(m) + 16 rows of slack make overflow negligible.
-    """
-    m = max(budget_frac * n - n_prot, 0.0)
-    c = budget_frac * n + 8.0 * math.sqrt(m + 1.0) + 16 + extra
-    c = min(int(math.ceil(c)), n + extra) if n > 0 else extra
-    return ((c + align - 1) // align) * align
-
-
 def bf16_bits(t: torch.Tensor):
     """bf16 tensor -> numpy uint16 bit patterns (host copy)."""
     return t.detach().to("cpu").contiguous().view(torch.int16).numpy().view("uint16")

@@ -1,0 +1,150 @@
+"""CPU checks of the C ABI: the library loads, exports every declared symbol, and rejects bad
+arguments synchronously (before any device work)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ebd.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*(ebd_[a-z_]+)\s*\(", src,
+                       flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for fn in ("ebd_evict", "ebd_attend_certify", "ebd_append_certain", "ebd_workspace_size",
+               "ebd_status_string", "ebd_version", "ebd_timing_enable", "ebd_timing_read"):
+        assert fn in names, fn
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2607_21475_amd as ebd
+
+    lib = ctypes.CDLL(ebd.LIB_PATH)
+    for fn in _declared_functions():
+        assert hasattr(lib, fn), fn
+
+
+def test_version_and_status_strings():
+    import paper_2607_21475_amd as ebd
+
+    assert ebd.ebd_version().startswith("ebd-gfx950")
+    for code in range(5):
+        assert isinstance(ebd.ebd_status_string(code), str)
+    assert ebd.ebd_status_string(99) == "unknown status"
+
+
+def _lib():
+    import paper_2607_21475_amd as ebd
+
+    return ebd, ebd._lib
+
+
+FAKE = 0x100000  # aligned, never dereferenced: validation fails before any device access
+
+
+def _evict_params(ebd, **kw):
+    p = ebd.ebd_evict_params()
+    p.num_units = kw.get("U", 4)
+    p.head_dim = kw.get("d", 128)
+    p.max_rows = kw.get("max_rows", 4096)
+    p.seq_off = FAKE
+    p.cap_off = FAKE
+    p.n_sink, p.n_recent = 4, 64
+    p.budget_frac = 0.1
+    p.pi_min = kw.get("pi_min", 0.01)
+    p.pi_mode = kw.get("pi_mode", 0)
+    return p
+
+
+def _call_evict(lib, p, ws_bytes=1 << 20, ws=FAKE, nulls=()):
+    ptrs = [FAKE] * 11
+    for i in nulls:
+        ptrs[i] = None
+    return lib.ebd_evict(ctypes.byref(p), *ptrs[:8], None, None, ptrs[10], ws, ws_bytes, None)
+
+
+def test_evict_argument_validation():
+    ebd, lib = _lib()
+    assert lib.ebd_evict(None, *([None] * 11), None, 0, None) == ebd.EBD_ERR_INVALID_ARG
+    assert _call_evict(lib, _evict_params(ebd, d=64)) == ebd.EBD_ERR_UNSUPPORTED
+    assert _call_evict(lib, _evict_params(ebd, pi_min=0.0)) == ebd.EBD_ERR_INVALID_ARG
+    assert _call_evict(lib, _evict_params(ebd, pi_min=1.5)) == ebd.EBD_ERR_INVALID_ARG
+    assert _call_evict(lib, _evict_params(ebd, pi_mode=2)) == ebd.EBD_ERR_INVALID_ARG
+    assert _call_evict(lib, _evict_params(ebd, U=-1)) == ebd.EBD_ERR_INVALID_ARG
+    assert _call_evict(lib, _evict_params(ebd), nulls=(0,)) == ebd.EBD_ERR_INVALID_ARG
+    assert _call_evict(lib, _evict_params(ebd), ws_bytes=16) == ebd.EBD_ERR_WORKSPACE
+    assert _call_evict(lib, _evict_params(ebd), ws=FAKE + 8) == ebd.EBD_ERR_WORKSPACE
+    assert _call_evict(lib, _evict_params(ebd), ws=None) == ebd.EBD_ERR_WORKSPACE
+    # misaligned K
+    p = _evict_params(ebd)
+    assert lib.ebd_evict(ctypes.byref(p), FAKE, FAKE + 2, *([FAKE] * 6), None, None, FAKE, FAKE,
+                         1 << 20, None) == ebd.EBD_ERR_INVALID_ARG
+    # zero units is a no-op
+    assert _call_evict(lib, _evict_params(ebd, U=0)) == ebd.EBD_OK
+
+
+def test_attend_argument_validation():
+    ebd, lib = _lib()
+
+    def params(**kw):
+        p = ebd.ebd_attend_params()
+        p.num_units = kw.get("U", 4)
+        p.group = kw.get("G", 7)
+        p.head_dim = kw.get("d", 128)
+        p.split_rows = kw.get("split", 0)
+        p.max_rows = kw.get("max_rows", 2000)
+        p.cap_off = FAKE
+        p.delta = kw.get("delta", 0.1)
+        p.flags = kw.get("flags", 0)
+        return p
+
+    def call(p, ws=FAKE, ws_bytes=1 << 30):
+        return lib.ebd_attend_certify(ctypes.byref(p), *([FAKE] * 10), ws, ws_bytes, None)
+
+    assert call(params(d=96)) == ebd.EBD_ERR_UNSUPPORTED
+    assert call(params(G=0)) == ebd.EBD_ERR_INVALID_ARG
+    assert call(params(split=100)) == ebd.EBD_ERR_INVALID_ARG
+    assert call(params(flags=1)) == ebd.EBD_ERR_INVALID_ARG
+    assert call(params(delta=1.0)) == ebd.EBD_ERR_INVALID_ARG
+    assert call(params(), ws_bytes=100) == ebd.EBD_ERR_WORKSPACE
+    assert call(params(U=0)) == ebd.EBD_OK
+
+
+def test_workspace_sizes():
+    ebd, lib = _lib()
+    p = _evict_params(ebd, U=1792, max_rows=6144)
+    n = ebd.ebd_workspace_size(ebd.EBD_WS_EVICT, p)
+    # lambda per unit + chunk offsets (3 chunks of 2048 per unit), each region 256-aligned
+    assert n == ((1792 * 4 + 255) // 256) * 256 + ((1792 * 3 * 4 + 255) // 256) * 256
+    a = ebd.ebd_attend_params()
+    a.num_units, a.group, a.head_dim, a.max_rows, a.cap_off = 1792, 7, 128, 1856, FAKE
+    a.delta = 0.1
+    m = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a)
+    assert m == 256 + 1792 * 2 * 7 * 288 * 4  # two splits of 1024 rows
+    assert lib.ebd_workspace_size(7, ctypes.byref(a)) == 0
+
+
+def test_binding_requires_gpu_tensors():
+    torch = pytest.importorskip("torch")
+    ebd, lib = _lib()
+    with pytest.raises(ValueError):
+        ebd._ptr(torch.zeros(4), torch.float32, "x")
+
+
+def test_no_oracle_in_product_path():
+    """The package never imports or loads the oracle (test infrastructure only)."""
+    pkg = os.path.join(ROOT, "paper_2607_21475_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".hpp", ".h")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in src.lower(), f

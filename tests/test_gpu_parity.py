@@ -1,0 +1,371 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the same inputs.
+
+Bars (stated in the design notes): pi within 1e-5 absolute; masks, compaction, counts and
+status bit-exact given the same fp32 pi (the GPU's pi is fed to the oracle's mask and
+compaction); yhat within 2e-3 relative (vector norm per query head); Vhat, b, r within 1e-2
+relative; ln Nhat within 1e-4 absolute.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import paper_2607_21475_amd  # noqa: F401  (fails loudly if libebd.so is missing)
+    yield
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _bits(t):
+    return synth.bf16_bits(t)
+
+
+def _inputs(lengths, seed=0, group=1, scores="window", bad=None):
+    K, V, seq_off = synth.make_cache(lengths, seed=seed, device="cuda")
+    if scores == "pareto":
+        sc = synth.pareto_scores(K.shape[0], seed=seed + 2, device="cuda")
+    else:
+        sc = synth.window_scores(K, seq_off, seed=seed + 2)
+    if bad is not None:
+        sc = sc.clone()
+        for i, v in bad:
+            sc[i] = v
+    q = synth.make_queries(len(lengths), group, seed=seed + 1, device="cuda")
+    return K, V, seq_off, sc, q
+
+
+def _evict(K, V, seq_off, sc, lengths, **kw):
+    from paper_2607_21475_amd import cache
+
+    out = cache.evict(K, V, sc, seq_off, lengths, want_pi=True, **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def _check_evict(lengths, K, V, seq_off, sc, out, n_sink=4, n_recent=64, budget=0.1, pi_min=0.01,
+                 seed=0, pi_mode=0, epoch=0):
+    Kb, Vb = _bits(K), _bits(V)
+    off = _np(seq_off)
+    coff = _np(out.cap_off)
+    s = _np(sc)
+    pi_gpu = _np(out.pi_full)[: off[-1]]
+    # (1) pi against the oracle's fp64 solve
+    ref = oracle.evict_batch(off, coff, s, Kb, Vb, n_sink, n_recent, budget_frac=budget,
+                             pi_min=pi_min, seed=seed, epoch=epoch, pi_mode=pi_mode)
+    assert np.max(np.abs(pi_gpu - ref["pi_full"]), initial=0.0) <= 1e-5
+    st_gpu = _np(out.status).astype(np.uint32) & ~np.uint32(oracle.ST_CAP_OVERFLOW)
+    st_ref = ref["status"] & ~np.uint32(oracle.ST_CAP_OVERFLOW)
+    np.testing.assert_array_equal(st_gpu, st_ref)
+    # (2) mask and compaction bit-exact given the GPU's pi
+    same = oracle.evict_batch(off, coff, s, Kb, Vb, n_sink, n_recent, pi_given=pi_gpu, seed=seed,
+                              epoch=epoch)
+    cnt = _np(out.count)
+    np.testing.assert_array_equal(cnt, same["count"])
+    np.testing.assert_array_equal(_np(out.status).astype(np.uint32) & oracle.ST_CAP_OVERFLOW,
+                                  same["status"] & oracle.ST_CAP_OVERFLOW)
+    Kc, Vc, pic, idx = _bits(out.Kc), _bits(out.Vc), _np(out.pic), _np(out.idxc)
+    for u in range(len(lengths)):
+        a = coff[u]
+        k = min(int(cnt[u]), int(coff[u + 1] - coff[u]))
+        np.testing.assert_array_equal(idx[a:a + k], same["idx"][a:a + k])
+        np.testing.assert_array_equal(pic[a:a + k].view(np.uint32), same["pic"][a:a + k].view(np.uint32))
+        np.testing.assert_array_equal(Kc[a:a + k], same["Kc"][a:a + k])
+        np.testing.assert_array_equal(Vc[a:a + k], same["Vc"][a:a + k])
+    # end-to-end masks from independently solved pi differ only on knife-edge tokens
+    diff = np.abs(cnt.astype(np.int64) - ref["count"].astype(np.int64)).sum()
+    assert diff <= max(2, int(2e-4 * off[-1]))
+    return cnt
+
+
+# ------------------------------------------------------------------------------------------
+# Sampler
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("lengths,budget", [
+    ([4096] * 8, 0.10),                       # single layer, 8 KV heads, context 4096
+    ([6144] * 6, 0.25),                       # 3 chunks per unit
+    ([0, 1, 5, 70, 100, 777, 2047, 2048, 2049, 4096, 5000, 6144, 9000, 16384], 0.2),  # ragged
+    ([20000, 40001, 3], 0.1),                 # longer than 16384: streamed scores
+])
+def test_evict_parity(lengths, budget):
+    _say("evict parity lengths=%s budget=%s" % (lengths[:6], budget))
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=3)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=budget, seed=11)
+    _check_evict(lengths, K, V, seq_off, sc, out, budget=budget, seed=11)
+
+
+def test_evict_pareto_scores_and_floor_0005():
+    lengths = [8192] * 4
+    _say("evict pareto")
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=5, scores="pareto")
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.1, pi_min=0.005, seed=2, epoch=3)
+    _check_evict(lengths, K, V, seq_off, sc, out, budget=0.1, pi_min=0.005, seed=2, epoch=3)
+
+
+def test_evict_literal_mode_and_protection():
+    lengths = [3000, 500, 64]
+    _say("evict literal mode")
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=6)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.3, n_sink=1, n_recent=7, pi_mode=1,
+                 seed=9)
+    _check_evict(lengths, K, V, seq_off, sc, out, n_sink=1, n_recent=7, budget=0.3, pi_mode=1,
+                 seed=9)
+
+
+def test_evict_degenerate_budgets_and_bad_scores():
+    lengths = [1000, 1000, 1000, 1000]
+    _say("evict degenerate")
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=7, bad=[(10, float("nan")), (20, float("inf")),
+                                                          (30, -3.0)])
+    sc = sc.clone()
+    sc[2000:3000] = 0.0  # unit 2: all scores zero
+    # per-unit budgets: floor binds (unit 0), normal, all-zero scores, nothing evicted (unit 3)
+    bpu = torch.tensor([0.07, 0.2, 0.3, 1.0], dtype=torch.float32, device="cuda")
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.0, budget_per_unit=bpu, pi_min=0.1,
+                 seed=4)
+    st = _np(out.status)
+    assert st[0] & oracle.ST_BUDGET_FLOOR and st[0] & oracle.ST_BAD_SCORE
+    assert st[3] & oracle.ST_NO_EVICTION
+    Kb, Vb = _bits(K), _bits(V)
+    off, coff = _np(seq_off), _np(out.cap_off)
+    ref = oracle.evict_batch(off, coff, _np(sc), Kb, Vb, 4, 64, budget_per_unit=_np(bpu),
+                             pi_min=0.1, seed=4)
+    np.testing.assert_array_equal(st.astype(np.uint32), ref["status"])
+    assert np.max(np.abs(_np(out.pi_full) - ref["pi_full"])) <= 1e-5
+
+
+def test_evict_capacity_overflow_is_flagged():
+    lengths = [4096, 4096]
+    _say("evict overflow")
+    from paper_2607_21475_amd import cache
+
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=8)
+    cap_host = [0, 128, 128 + 4096]  # unit 0 far too small, unit 1 roomy
+    out = cache.evict(K, V, sc, seq_off, lengths, budget_frac=0.25, seed=1, cap_off_host=cap_host,
+                      want_pi=True)
+    torch.cuda.synchronize()
+    st = _np(out.status)
+    cnt = _np(out.count)
+    assert st[0] & oracle.ST_CAP_OVERFLOW and not st[1] & oracle.ST_CAP_OVERFLOW
+    assert cnt[0] > 128
+    same = oracle.evict_batch(_np(seq_off), np.array(cap_host, np.int64), _np(sc), _bits(K), _bits(V),
+                              4, 64, pi_given=_np(out.pi_full), seed=1)
+    np.testing.assert_array_equal(cnt, same["count"])
+    np.testing.assert_array_equal(_bits(out.Kc)[:128], same["Kc"][:128])
+    np.testing.assert_array_equal(_np(out.idxc)[:128], same["idx"][:128])
+
+
+def test_evict_deterministic():
+    lengths = [6144] * 4
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=9)
+    a = _evict(K, V, seq_off, sc, lengths, budget_frac=0.25, seed=5)
+    b = _evict(K, V, seq_off, sc, lengths, budget_frac=0.25, seed=5)
+    assert torch.equal(a.count, b.count) and torch.equal(a.pi_full, b.pi_full)
+    coff = _np(a.cap_off)
+    cnt = _np(a.count)
+    for u in range(len(lengths)):  # rows past count are unwritten capacity
+        r = slice(int(coff[u]), int(coff[u] + cnt[u]))
+        assert torch.equal(a.Kc[r].view(torch.int16), b.Kc[r].view(torch.int16))
+        assert torch.equal(a.Vc[r].view(torch.int16), b.Vc[r].view(torch.int16))
+        assert torch.equal(a.idxc[r], b.idxc[r]) and torch.equal(a.pic[r], b.pic[r])
+    c = _evict(K, V, seq_off, sc, lengths, budget_frac=0.25, seed=5, epoch=1)
+    k = int(min(a.count[0], c.count[0]))
+    assert not torch.equal(a.idxc[:k], c.idxc[:k])
+
+
+# ------------------------------------------------------------------------------------------
+# Certified attention
+# ------------------------------------------------------------------------------------------
+def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
+    coff = _np(out.cap_off)
+    cnt = _np(out.count)
+    ref = oracle.attend_batch(coff, cnt, _bits(q), _bits(out.Kc), _bits(out.Vc), _np(out.pic))
+    y, yr = _np(res["y"]).astype(np.float64), ref["y"]
+    nrm = np.linalg.norm(yr, axis=2)
+    err = np.linalg.norm(y - yr, axis=2)
+    empty = cnt == 0
+    assert np.all(err[~empty] <= tol_y * nrm[~empty]), np.max(err[~empty] / nrm[~empty])
+    assert np.all(y[empty] == 0)
+    for key in ("vhat", "b", "r"):
+        g, r = _np(res[key]).astype(np.float64), ref[key]
+        floor = 1e-6 * (nrm ** 2 if key == "vhat" else nrm) + 1e-30
+        bad = np.abs(g - r) > tol_c * np.maximum(np.abs(r), floor)
+        assert not bad.any(), (key, np.argwhere(bad)[:5], g[bad][:5], r[bad][:5])
+    lse, lr = _np(res["lse"]).astype(np.float64), ref["lse"]
+    assert np.all(np.isneginf(lse[empty]))
+    assert np.all(np.abs(lse[~empty] - lr[~empty]) <= 1e-4 * np.maximum(1.0, np.abs(lr[~empty])))
+    return ref
+
+
+@pytest.mark.parametrize("lengths,G,budget,split", [
+    ([4096] * 8, 1, 0.10, 0),                  # single layer, G = 1
+    ([6144] * 8, 7, 0.25, 0),                  # GQA 7
+    ([6144] * 8, 7, 0.25, 64),                 # many splits per unit
+    ([16384] * 4, 4, 0.25, 0),                 # GQA 4, long cache
+    ([2048, 777, 100, 5, 9000, 3000], 8, 0.3, 128),  # ragged tails, G = 8
+    ([3000, 1500], 12, 0.2, 0),                # two head blocks (8 + 4)
+    ([4096, 300], 9, 0.5, 256),                # 8 + 1
+])
+def test_attend_parity(lengths, G, budget, split):
+    _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))
+    from paper_2607_21475_amd import cache
+
+    K, V, seq_off, sc, q = _inputs(lengths, seed=13, group=G)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=budget, seed=21)
+    res = cache.attend_certify(out, q, split_rows=split)
+    torch.cuda.synchronize()
+    _check_attend(out, res, q, G)
+
+
+def test_attend_empty_and_tiny_units():
+    _say("attend empty units")
+    from paper_2607_21475_amd import cache
+
+    lengths = [0, 1, 2, 17, 64, 65]
+    K, V, seq_off, sc, q = _inputs(lengths, seed=14, group=3)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.3, n_sink=0, n_recent=1, seed=2)
+    res = cache.attend_certify(out, q)
+    torch.cuda.synchronize()
+    assert _np(out.count)[0] == 0
+    _check_attend(out, res, q, 3)
+
+
+def test_attend_range_term_rescan_path():
+    """Values with equal norms and equal weights: candidate bounds cannot decide, so splits are
+    rescanned; b must still equal the oracle's exact maximum."""
+    _say("attend rescan path")
+    from paper_2607_21475_amd import cache
+
+    U, n, G = 4, 2048, 2
+    lengths = [n] * U
+    K = torch.zeros((U * n, 128), dtype=torch.bfloat16, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    sign = torch.randint(0, 2, (U * n, 128), generator=g, device="cuda").float() * 2 - 1
+    V = sign.to(torch.bfloat16)  # every |v| = sqrt(128)
+    seq_off = synth.seq_offsets(lengths, "cuda")
+    sc = torch.ones(U * n, dtype=torch.float32, device="cuda")
+    q = synth.make_queries(U, G, seed=4, device="cuda")
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.2, seed=8)
+    res = cache.attend_certify(out, q, split_rows=128)
+    torch.cuda.synchronize()
+    assert cache.rescans(res["ws"]) > 0
+    _check_attend(out, res, q, G)
+
+
+def test_attend_pi_one_is_full_attention():
+    """Budget 1: nothing evicted, pi = 1 everywhere, so yhat is full attention and Vhat = b = r = 0."""
+    _say("attend pi=1")
+    from paper_2607_21475_amd import cache
+
+    lengths = [3000, 1000]
+    K, V, seq_off, sc, q = _inputs(lengths, seed=15, group=4)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=1.0, seed=1)
+    res = cache.attend_certify(out, q)
+    torch.cuda.synchronize()
+    yfull = oracle.full_batch(_np(seq_off), _bits(q), _bits(K), _bits(V))
+    err = np.linalg.norm(_np(res["y"]) - yfull, axis=2) / np.linalg.norm(yfull, axis=2)
+    assert np.max(err) <= 2e-3
+    assert np.all(_np(res["vhat"]) == 0) and np.all(_np(res["b"]) == 0) and np.all(_np(res["r"]) == 0)
+
+
+def test_append_certain():
+    _say("append")
+    from paper_2607_21475_amd import cache, ebd_append_certain
+
+    lengths = [1000, 1000, 1000]
+    K, V, seq_off, sc, q = _inputs(lengths, seed=16, group=2)
+    cap_host = cache.plan_capacity(lengths, 0.1, 4, 64, extra=2)
+    out = cache.evict(K, V, sc, seq_off, lengths, budget_frac=0.1, seed=3, cap_off_host=cap_host)
+    torch.cuda.synchronize()
+    c0 = _np(out.count).copy()
+    kn = synth.make_queries(3, 1, seed=30, device="cuda")[:, 0].contiguous()
+    vn = synth.make_queries(3, 1, seed=31, device="cuda")[:, 0].contiguous()
+    pos = torch.tensor([1000, 1000, 1000], dtype=torch.int32, device="cuda")
+    ebd_append_certain(3, out.cap_off, out.count, kn, vn, out.Kc, out.Vc, out.pic, out.idxc, pos,
+                       out.status)
+    torch.cuda.synchronize()
+    c1 = _np(out.count)
+    np.testing.assert_array_equal(c1, c0 + 1)
+    coff = _np(out.cap_off)
+    for u in range(3):
+        r = coff[u] + c0[u]
+        np.testing.assert_array_equal(_bits(out.Kc)[r], _bits(kn)[u])
+        np.testing.assert_array_equal(_bits(out.Vc)[r], _bits(vn)[u])
+        assert _np(out.pic)[r] == 1.0 and _np(out.idxc)[r] == 1000
+    res = cache.attend_certify(out, q)
+    torch.cuda.synchronize()
+    _check_attend(out, res, q, 2)
+    # fill unit 0 to capacity: the next append is refused and flagged
+    room = int(coff[1] - coff[0] - c1[0])
+    for _ in range(room):
+        ebd_append_certain(3, out.cap_off, out.count, kn, vn, out.Kc, out.Vc, out.pic, out.idxc, pos,
+                           out.status)
+    ebd_append_certain(3, out.cap_off, out.count, kn, vn, out.Kc, out.Vc, out.pic, out.idxc, pos,
+                       out.status)
+    torch.cuda.synchronize()
+    assert _np(out.count)[0] == coff[1] - coff[0]
+    assert _np(out.status)[0] & oracle.ST_CAP_OVERFLOW
+
+
+# ------------------------------------------------------------------------------------------
+# Full-size workload (the benchmark's launch configuration), sampled units
+# ------------------------------------------------------------------------------------------
+def test_qwen7b_full_size_sampled_units():
+    wl = synth.WORKLOADS["qwen7b_6k"]
+    _say("full-size %s U=%d" % (wl.name, wl.units))
+    from paper_2607_21475_amd import cache
+
+    inp = synth.make_workload_inputs(wl, seed=0, device="cuda")
+    lengths = [wl.context] * wl.units
+    rng = np.random.default_rng(0)
+    sample = np.sort(rng.choice(wl.units, 12, replace=False))
+    for budget in wl.budgets:
+        out = cache.evict(inp["K"], inp["V"], inp["scores"], inp["seq_off"], lengths,
+                          budget_frac=budget, n_sink=wl.n_sink, n_recent=wl.n_recent,
+                          pi_min=wl.pi_min, seed=0, want_pi=True)
+        res = cache.attend_certify(out, inp["q"])
+        torch.cuda.synchronize()
+        assert not (_np(out.status) & oracle.ST_CAP_OVERFLOW).any()
+        n = wl.context
+        cnt = _np(out.count)
+        coff = _np(out.cap_off)
+        pi_all = _np(out.pi_full)
+        for u in sample:
+            sl = slice(u * n, (u + 1) * n)
+            s = _np(inp["scores"][sl])
+            Kb, Vb = _bits(inp["K"][sl]), _bits(inp["V"][sl])
+            pi_ref, lam, st = oracle.inclusion_probs(s, wl.n_sink, wl.n_recent, budget, wl.pi_min)
+            assert np.max(np.abs(pi_all[sl] - pi_ref)) <= 1e-5
+            m = oracle.mask(pi_all[sl], 0, int(u), 0)
+            Kc_r, Vc_r, pic_r, idx_r, c_r = oracle.compact(m, pi_all[sl], Kb, Vb)
+            assert c_r == cnt[u]
+            a = coff[u]
+            np.testing.assert_array_equal(_np(out.idxc)[a:a + c_r], idx_r)
+            np.testing.assert_array_equal(_bits(out.Kc[a:a + c_r]), Kc_r)
+            np.testing.assert_array_equal(_bits(out.Vc[a:a + c_r]), Vc_r)
+            ref = oracle.attend_certify(_bits(inp["q"][u]), Kc_r, Vc_r, pic_r)
+            y = _np(res["y"][u]).astype(np.float64)
+            assert np.all(np.linalg.norm(y - ref["y"], axis=1) <= 2e-3 * np.linalg.norm(ref["y"], axis=1))
+            for key in ("vhat", "b", "r"):
+                g = _np(res[key][u]).astype(np.float64)
+                assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.abs(ref[key])), (key, u, g, ref[key])
+        del out, res
+    del inp
+    torch.cuda.empty_cache()
