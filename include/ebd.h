@@ -51,8 +51,8 @@ typedef enum ebd_status {
                                   of them get pi = 1 (zero scores keep pi_min) */
 #define EBD_ST_BAD_SCORE 8u    /* a NaN, infinite or negative score was seen; it is
                                   treated as 0 (pi = pi_min) */
-#define EBD_ST_BAD_LAYOUT 16u  /* the unit has more rows than params.max_rows: nothing was
-                                  sampled or written for it and count[u] = 0 */
+#define EBD_ST_BAD_LAYOUT 16u  /* the unit exceeds params.max_rows or params.max_capacity:
+                                  nothing was sampled or written for it and count[u] = 0 */
 
 /*
  * Sampler parameters (Sec. 3.3, eq. (2) and the certainty set).
@@ -60,7 +60,10 @@ typedef enum ebd_status {
  *            of `scores`, `K`, `V` (non-decreasing; uniform caches: u * n).
  *   cap_off  [U+1] device int64: unit u owns compacted rows cap_off[u] .. cap_off[u+1]-1
  *            of Kc, Vc, pic, idxc (its capacity).
- *   max_rows host value >= max_u (seq_off[u+1] - seq_off[u]); sizes the launch grid.
+ *   max_rows host value >= max_u (seq_off[u+1] - seq_off[u]); units longer than this are
+ *            flagged EBD_ST_BAD_LAYOUT and left untouched.
+ *   max_capacity host value >= max_u (cap_off[u+1] - cap_off[u]); sizes the copy grid.
+ *            Units outside either bound are flagged EBD_ST_BAD_LAYOUT (nothing written).
  *   n_sink, n_recent: protected positions i < n_sink and i >= n - n_recent (pi = 1).
  *   budget_frac f: expected resident tokens per unit = f * n, protected ones included,
  *            so the tail budget is m = f n - |P| (real valued).
@@ -76,6 +79,7 @@ typedef struct ebd_evict_params {
     int32_t num_units;
     int32_t head_dim;
     int64_t max_rows;
+    int64_t max_capacity;
     const int64_t *seq_off;
     const int64_t *cap_off;
     int32_t n_sink;
@@ -100,7 +104,8 @@ typedef struct ebd_evict_params {
  *     lambda_out [U] fp32 or NULL   the solved scale (+inf when nothing is evicted)
  *     pi_full [rows] fp32 or NULL   pi of every full-cache position
  *     status [U] uint32             EBD_ST_* bits
- *   workspace: at least ebd_workspace_size(EBD_WS_EVICT, p) bytes, 256-byte aligned.
+ *   workspace: at least ebd_workspace_size(EBD_WS_EVICT, p) bytes, 256-byte aligned
+ *   (currently reserved: the two sampler launches share only the idxc list they write).
  *   Rows of Kc/Vc/pic/idxc beyond count[u] are left untouched.
  */
 ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint16_t *K,
@@ -183,8 +188,8 @@ const char *ebd_version(void);
 /*
  * Kernel timing (profiling aid).  While enabled, every kernel launch of the library is
  * bracketed by HIP events recorded on the launch stream.  ebd_timing_read() waits for the
- * recorded events, and adds the elapsed times of kernel `name` ("evict_solve",
- * "evict_compact", "attend_split", "attend_finalize", "append_certain") to *total_ms and
+ * recorded events, and adds the elapsed times of kernel `name` ("evict_select",
+ * "evict_copy", "attend_split", "attend_finalize", "append_certain") to *total_ms and
  * its launch count to *launches; it then clears that kernel's record.  Not meant for use
  * from several host threads at once.
  */

@@ -50,6 +50,7 @@ class ebd_evict_params(ctypes.Structure):
         ("num_units", ctypes.c_int32),
         ("head_dim", ctypes.c_int32),
         ("max_rows", ctypes.c_int64),
+        ("max_capacity", ctypes.c_int64),
         ("seq_off", ctypes.c_void_p),
         ("cap_off", ctypes.c_void_p),
         ("n_sink", ctypes.c_int32),
@@ -139,13 +140,14 @@ def ebd_version() -> str:
     return _lib.ebd_version().decode()
 
 
-def evict_params(num_units, max_rows, seq_off, cap_off, n_sink=4, n_recent=64, budget_frac=0.1,
-                 budget_per_unit=None, pi_min=0.01, pi_mode=0, seed=0, seed_per_unit=None,
-                 epoch=0) -> ebd_evict_params:
+def evict_params(num_units, max_rows, max_capacity, seq_off, cap_off, n_sink=4, n_recent=64,
+                 budget_frac=0.1, budget_per_unit=None, pi_min=0.01, pi_mode=0, seed=0,
+                 seed_per_unit=None, epoch=0) -> ebd_evict_params:
     p = ebd_evict_params()
     p.num_units = int(num_units)
     p.head_dim = HEAD_DIM
     p.max_rows = int(max_rows)
+    p.max_capacity = int(max_capacity)
     p.seq_off = _ptr(seq_off, torch.int64, "seq_off")
     p.cap_off = _ptr(cap_off, torch.int64, "cap_off")
     p.n_sink = int(n_sink)

@@ -88,8 +88,9 @@ def evict(K: torch.Tensor, V: torch.Tensor, scores: torch.Tensor, seq_off: torch
         lam=torch.empty((U,), dtype=torch.float32, device=dev),
         pi_full=torch.empty((max(K.shape[0], 1),), dtype=torch.float32, device=dev) if want_pi else None,
     )
-    p = evict_params(U, max(lengths) if lengths else 0, seq_off, cap_off, n_sink, n_recent,
-                     budget_frac, budget_per_unit, pi_min, pi_mode, seed, seed_per_unit, epoch)
+    p = evict_params(U, max(lengths) if lengths else 0, out.max_cap, seq_off, cap_off, n_sink,
+                     n_recent, budget_frac, budget_per_unit, pi_min, pi_mode, seed, seed_per_unit,
+                     epoch)
     ws = workspace(ebd_workspace_size(EBD_WS_EVICT, p), dev)
     ebd_evict(p, scores, K, V, out.Kc, out.Vc, out.pic, out.idxc, out.count, out.status, ws,
               lambda_out=out.lam, pi_full=out.pi_full)

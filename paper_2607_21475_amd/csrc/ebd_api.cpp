@@ -78,17 +78,8 @@ hipError_t timed(const char *name, hipStream_t s, F &&launch) {
   return hipSuccess;
 }
 
-int32_t evict_chunks(int64_t max_rows) {
-  return (int32_t)((max_rows + kEvictChunk - 1) / kEvictChunk);
-}
-
-int32_t evict_reg_chunks(int32_t nchunk) {
-  if (nchunk <= 1) return 1;
-  if (nchunk <= 2) return 2;
-  if (nchunk <= 4) return 4;
-  if (nchunk <= kEvictRegChunks) return 8;
-  return 0;
-}
+// The sampler keeps no state between its two launches except the index list it writes.
+constexpr size_t kEvictWorkspace = 256;
 
 // Rows per split: at most 1024, halved (down to 256) until the grid has >= 2048 work-groups
 // (eight per compute unit), unless the caller fixes it.
@@ -111,6 +102,7 @@ int32_t attend_nsplit(const ebd_attend_params *p, int32_t sr) {
 bool valid_evict_params(const ebd_evict_params *p) {
   if (!p) return false;
   if (p->num_units < 0 || p->max_rows < 0 || p->max_rows > ((int64_t)1 << 31)) return false;
+  if (p->max_capacity < 0 || p->max_capacity > ((int64_t)1 << 31)) return false;
   if (p->num_units > 0 && (!p->seq_off || !p->cap_off)) return false;
   if (p->n_sink < 0 || p->n_recent < 0) return false;
   if (!(p->pi_min > 0.0f && p->pi_min <= 1.0f)) return false;
@@ -154,7 +146,7 @@ size_t ebd_workspace_size(int32_t which, const void *params) {
   if (which == EBD_WS_EVICT) {
     const ebd_evict_params *p = static_cast<const ebd_evict_params *>(params);
     if (!valid_evict_params(p)) return 0;
-    return evict_workspace_bytes(p->num_units, evict_chunks(p->max_rows));
+    return kEvictWorkspace;
   }
   if (which == EBD_WS_ATTEND) {
     const ebd_attend_params *p = static_cast<const ebd_attend_params *>(params);
@@ -177,16 +169,15 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) ||
       !aligned(scores, 4) || !aligned(pic, 4) || !aligned(idxc, 4))
     return EBD_ERR_INVALID_ARG;
-  const int32_t nchunk = evict_chunks(p->max_rows);
-  const size_t need = evict_workspace_bytes(p->num_units, nchunk);
-  if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
+  if (!workspace || ws_bytes < kEvictWorkspace || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
   const ebd_status ds = check_device();
   if (ds != EBD_OK) return ds;
 
   EvictLaunch L;
   L.U = p->num_units;
-  L.nchunk = nchunk > 0 ? nchunk : 1;
-  L.reg_chunks = evict_reg_chunks(nchunk);
+  L.max_rows = p->max_rows;
+  L.stage_rows = p->max_rows <= kEvictStageMax ? p->max_rows : 0;
+  L.copy_blocks = (int32_t)((p->max_capacity + kCopyRows - 1) / kCopyRows);
   L.seq_off = p->seq_off;
   L.cap_off = p->cap_off;
   L.n_sink = p->n_sink;
@@ -209,15 +200,11 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
   L.lambda_out = lambda_out;
   L.pi_full = pi_full;
   L.status = status;
-  char *ws = static_cast<char *>(workspace);
-  L.ws_lambda = reinterpret_cast<float *>(ws);
-  L.ws_chunk_off = reinterpret_cast<int32_t *>(ws + (((size_t)L.U * sizeof(float) + 255) & ~(size_t)255));
-
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (timed("evict_solve", s, [&] { return launch_evict_solve(L, s); }) != hipSuccess)
+  if (timed("evict_select", s, [&] { return launch_evict_select(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
-  if (p->max_rows > 0 &&
-      timed("evict_compact", s, [&] { return launch_evict_compact(L, s); }) != hipSuccess)
+  if (L.copy_blocks > 0 &&
+      timed("evict_copy", s, [&] { return launch_evict_copy(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
   return EBD_OK;
 }

@@ -8,29 +8,32 @@
 namespace ebd {
 
 constexpr int kHeadDim = 128;                // rows of K, V and q are 128 bf16
-constexpr int kEvictThreads = 512;            // one work-group per (unit, chunk)
-constexpr int kEvictChunk = 4 * kEvictThreads;  // tokens per chunk: four per thread (one Philox block)
-constexpr int kEvictRegChunks = 8;            // scores held in registers up to 8 chunks (16384 tokens)
+constexpr int kEvictStageMax = 16384;        // scores staged in LDS (64 KB) up to this length
+constexpr int kSelectThreads = 256;          // evict_select: four waves per unit
+constexpr int kCopyThreads = 256;            // evict_copy: 16 lanes per 256-byte row
+constexpr int kCopyRows = 128;               // retained rows per evict_copy work-group
 
 constexpr int kAttendThreads = 256;  // four waves per (unit, split, head block)
 constexpr int kHeadBlock = 8;        // query heads handled together (MFMA rows: 8 weight + 8 variance)
-constexpr int kCand = 8;             // range-term candidates kept per (split, head)
-constexpr int kRec = 288;            // floats per (unit, split, head) partial record
+constexpr int kCand = 32;            // range-term candidates kept per (split, head)
+constexpr int kRec = 328;            // floats per (unit, split, head) partial record
 
-// Partial record layout (floats):
-//   [0] m  running logit max        [1] l  = sum w        (scale e^{-m})
-//   [2] C0 = sum c                  [3] C2 = sum c |v|^2  (scale e^{-2m})
+// Partial record layout (floats), logits in base 2:
+//   [0] m  running logit max        [1] l  = sum w        (scale 2^{-m})
+//   [2] C0 = sum c                  [3] C2 = sum c |v|^2  (scale 2^{-2m})
 //   [4] A  max over non-candidates of g |v|   [5] B  max over non-candidates of g
-//   [8..15] candidate g             [16..23] candidate row (int bits, -1 = none)
-//   [24..151] o = sum w v           [152..279] Cv = sum c v
-//   with w = exp(l - m), c = (1 - pi) w^2, g = sqrt(1 - pi) w.
-constexpr int kRecM = 0, kRecL = 1, kRecC0 = 2, kRecC2 = 3, kRecA = 4, kRecB = 5;
-constexpr int kRecCandG = 8, kRecCandI = 16, kRecO = 24, kRecCv = 152;
+//   [6] Vmax  max |v| over the candidates
+//   [8..39] candidate g             [40..71] candidate row (int bits, -1 = none)
+//   [72..199] o = sum w v           [200..327] Cv = sum c v
+//   with w = 2^(l2 - m), c = (1 - pi) w^2, g = sqrt(1 - pi) w.
+constexpr int kRecM = 0, kRecL = 1, kRecC0 = 2, kRecC2 = 3, kRecA = 4, kRecB = 5, kRecVmax = 6;
+constexpr int kRecCandG = 8, kRecCandI = 40, kRecO = 72, kRecCv = 200;
 
 struct EvictLaunch {
   int32_t U;
-  int32_t nchunk;  // chunks per unit in the compact grid = ceil(max_rows / kEvictChunk)
-  int32_t reg_chunks;  // 1, 2, 4, 8: scores in registers; 0: streamed from memory
+  int64_t max_rows;     // longest unit the launch was planned for
+  int64_t stage_rows;   // LDS staging length of evict_select (0: scores streamed from memory)
+  int32_t copy_blocks;  // evict_copy work-groups per unit = ceil(max capacity / kCopyRows)
   const int64_t *seq_off;
   const int64_t *cap_off;
   int32_t n_sink, n_recent;
@@ -50,8 +53,6 @@ struct EvictLaunch {
   float *lambda_out;
   float *pi_full;
   uint32_t *status;
-  float *ws_lambda;        // [U]
-  int32_t *ws_chunk_off;   // [U * nchunk]
 };
 
 struct AttendLaunch {
@@ -78,11 +79,10 @@ struct AppendLaunch {
   uint32_t *status;
 };
 
-size_t evict_workspace_bytes(int32_t U, int32_t nchunk);
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G);
 
-hipError_t launch_evict_solve(const EvictLaunch &L, hipStream_t s);
-hipError_t launch_evict_compact(const EvictLaunch &L, hipStream_t s);
+hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s);
+hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s);
 hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_attend_finalize(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_append_certain(const AppendLaunch &L, hipStream_t s);

@@ -2,14 +2,17 @@
 // Sec. 3.1: evicted rows are deleted, retained rows keep one stored pi each).
 //
 // Two launches per call:
-//   evict_solve    one work-group per unit.  Reads the unit's scores once (kept in registers
-//                  up to 16384 tokens), solves lambda with sum_T clip(lambda s, eps, 1) = m, then
-//                  draws the mask once to count retained tokens per 2048-token chunk and writes
-//                  the chunk offsets, count and status.
-//   evict_compact  one work-group per (unit, chunk).  Recomputes pi and the Philox words of its
-//                  2048 tokens (bit-identical to the solve pass), ranks the retained ones with a
-//                  block scan and copies only the retained K/V rows (16 lanes x 16 B per row).
-//                  Evicted rows are never read.
+//   evict_select  one work-group (4 waves) per unit.  Stages the unit's scores in LDS (up to
+//                 16384 tokens, protected positions marked by a negative sentinel; longer units
+//                 are re-read from memory), solves lambda with sum_T clip(lambda s, eps, 1) = m by
+//                 safeguarded Newton steps on the piecewise linear g(lambda) (exact once the
+//                 piece is found), then walks the unit in 1024-token blocks: Philox words, exact
+//                 retention test, ballot ranks plus a cross-wave prefix, and writes the stored pi
+//                 and original position of every retained row in order, plus the count and the
+//                 status bits.
+//   evict_copy    one work-group per (unit, block of retained rows): gathers the retained K and
+//                 V rows named by the index list (16 lanes x 16 B per 256-byte row, all loads of
+//                 a thread in flight together).  Evicted rows are never read.
 #include "ebd.h"
 #include "ebd_device.hpp"
 #include "ebd_internal.hpp"
@@ -17,10 +20,6 @@
 namespace ebd {
 
 namespace {
-
-__device__ __forceinline__ bool in_tail(int64_t i, int64_t n, int32_t n_sink, int32_t n_recent) {
-  return i >= (int64_t)n_sink && i < n - (int64_t)n_recent;
-}
 
 // Non-finite and negative scores are read as 0 and flagged.
 __device__ __forceinline__ float clean_score(float s, uint32_t &bad) {
@@ -31,170 +30,167 @@ __device__ __forceinline__ float clean_score(float s, uint32_t &bad) {
   return s;
 }
 
-// pi of one position; used identically by both launches so their masks agree bit for bit.
 __device__ __forceinline__ float token_pi(bool tail, float s, float lam, float eps) {
   if (!tail) return 1.0f;
   if (isinf(lam)) return s > 0.0f ? 1.0f : eps;
   return fminf(fmaxf(lam * s, eps), 1.0f);
 }
 
-__device__ __forceinline__ uint64_t unit_seed(const EvictLaunch &L, int u) {
-  return L.seed_per_unit ? L.seed_per_unit[u] : L.seed;
+// Block-wide sums over the 256 threads of evict_select (4 waves).  `buf` alternates between
+// calls so that one barrier per call suffices.
+struct BlockRed {
+  double v[2][4][4];
+};
+
+__device__ __forceinline__ double wave_sum_d(double x) {
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
 }
 
-// Sum of three doubles over the 512-thread block; every thread gets the totals.
-// `buf` alternates between calls so one barrier per call suffices.
-__device__ __forceinline__ void block_sum3(double &a, double &b, double &c, double (*red)[8][3],
-                                           int &buf) {
+// Sums a, b, c (each exact in double for counts) over the block; all threads get the totals.
+__device__ __forceinline__ void block_sum3(double &a, double &b, double &c, BlockRed &R, int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  a = wave_sum(a);
-  b = wave_sum(b);
-  c = wave_sum(c);
+  a = wave_sum_d(a);
+  b = wave_sum_d(b);
+  c = wave_sum_d(c);
   if (lane == 0) {
-    red[buf][wv][0] = a;
-    red[buf][wv][1] = b;
-    red[buf][wv][2] = c;
+    R.v[buf][wv][0] = a;
+    R.v[buf][wv][1] = b;
+    R.v[buf][wv][2] = c;
   }
   __syncthreads();
-  a = b = c = 0.0;
-#pragma unroll
-  for (int w = 0; w < kEvictThreads / 64; ++w) {
-    a += red[buf][w][0];
-    b += red[buf][w][1];
-    c += red[buf][w][2];
-  }
+  a = R.v[buf][0][0] + R.v[buf][1][0] + R.v[buf][2][0] + R.v[buf][3][0];
+  b = R.v[buf][0][1] + R.v[buf][1][1] + R.v[buf][2][1] + R.v[buf][3][1];
+  c = R.v[buf][0][2] + R.v[buf][1][2] + R.v[buf][2][2] + R.v[buf][3][2];
   buf ^= 1;
 }
 
-__device__ __forceinline__ void block_minmax(float &mx, float &mn, float (*red)[8][2], int &buf) {
+__device__ __forceinline__ void block_minmax(float &mx, float &mn, BlockRed &R, int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   mx = wave_max(mx);
   mn = wave_min(mn);
   if (lane == 0) {
-    red[buf][wv][0] = mx;
-    red[buf][wv][1] = mn;
+    R.v[buf][wv][0] = (double)mx;
+    R.v[buf][wv][1] = (double)mn;
   }
   __syncthreads();
-#pragma unroll
-  for (int w = 0; w < kEvictThreads / 64; ++w) {
-    mx = fmaxf(mx, red[buf][w][0]);
-    mn = fminf(mn, red[buf][w][1]);
+  for (int w = 0; w < 4; ++w) {
+    mx = fmaxf(mx, (float)R.v[buf][w][0]);
+    mn = fminf(mn, (float)R.v[buf][w][1]);
   }
   buf ^= 1;
-}
-
-// Scores of the thread's four-token groups: group k covers tokens 4 (t + 512 k) .. +3.
-template <int RC>
-struct ScoreRegs {
-  float v[RC > 0 ? RC : 1][4];
-};
-
-template <int RC>
-__device__ __forceinline__ void load_group(const float *sc, int64_t n, int64_t gi, float (&s)[4],
-                                           uint32_t &bad) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t i = 4 * gi + j;
-    s[j] = i < n ? clean_score(sc[i], bad) : 0.0f;
-  }
 }
 
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
-// evict_solve: lambda, per-chunk retained counts, count, status
+// evict_select: lambda, mask, stored pi and index of every retained row, count, status
 // ---------------------------------------------------------------------------------------------
-template <int RC>
-__global__ __launch_bounds__(kEvictThreads) void evict_solve_kernel(EvictLaunch L) {
-  __shared__ double red3[2][8][3];
-  __shared__ float red2[2][8][2];
-  int b3 = 0, b2 = 0;
+__global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunch L) {
+  extern __shared__ float s_sc[];
+  __shared__ BlockRed R;
+  __shared__ int s_tot[2][kSelectThreads / 64];
+  int rbuf = 0;
   const int u = blockIdx.x;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int64_t base = L.seq_off[u];
   const int64_t n = L.seq_off[u + 1] - base;
-  const int64_t cap = L.cap_off[u + 1] - L.cap_off[u];
+  const int64_t cbase = L.cap_off[u];
+  const int64_t cap = L.cap_off[u + 1] - cbase;
+  if (n > L.max_rows || cap > (int64_t)L.copy_blocks * kCopyRows) {
+    // larger than the launch was planned for: touch nothing of this unit
+    if (t == 0) {
+      L.count[u] = 0;
+      L.status[u] = EBD_ST_BAD_LAYOUT;
+      if (L.lambda_out) L.lambda_out[u] = 0.0f;
+    }
+    return;
+  }
   const int64_t nprot = min(n, (int64_t)L.n_sink + (int64_t)L.n_recent);
   const double f = L.budget_per_unit ? (double)L.budget_per_unit[u] : (double)L.budget_frac;
   const double m = f * (double)n - (double)nprot;
   const float eps = L.pi_min;
   const float *sc = L.scores + base;
   const int64_t ngroups = (n + 3) / 4;
-  if ((n + kEvictChunk - 1) / kEvictChunk > (int64_t)L.nchunk) {
-    // longer than the launch was planned for: touch nothing of this unit
-    if (t == 0) {
-      L.count[u] = 0;
-      L.status[u] = EBD_ST_BAD_LAYOUT;
-      L.ws_lambda[u] = 0.0f;
-      if (L.lambda_out) L.lambda_out[u] = 0.0f;
-    }
-    return;
-  }
+  const int64_t tail_lo = L.n_sink, tail_hi = n - (int64_t)L.n_recent;  // T = [tail_lo, tail_hi)
+  const bool staged = L.stage_rows > 0;
+  const bool vec = ((base & 3) == 0);  // 16-byte aligned score groups
 
-  ScoreRegs<RC> R;
-  uint32_t bad = 0;
-  if (RC > 0) {
+  // Raw scores of group gi (0 past the end).
+  auto load_raw = [&](int64_t gi) -> float4 {
+    const int64_t i = 4 * gi;
+    if (vec && i + 3 < n) return reinterpret_cast<const float4 *>(sc)[gi];
+    float4 r;
+    r.x = i < n ? sc[i] : 0.0f;
+    r.y = i + 1 < n ? sc[i + 1] : 0.0f;
+    r.z = i + 2 < n ? sc[i + 2] : 0.0f;
+    r.w = i + 3 < n ? sc[i + 3] : 0.0f;
+    return r;
+  };
+  // Cleaned tail scores of group gi; positions outside T (protected or past the end) read -1.
+  auto tail4 = [&](int64_t gi, float4 raw, uint32_t &bad) -> float4 {
+    float v[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
-    for (int k = 0; k < (RC > 0 ? RC : 1); ++k) load_group<RC>(sc, n, t + (int64_t)kEvictThreads * k, R.v[k], bad);
-  }
-
-  // Visit every token of the thread: f(i, s).
-  auto for_tokens = [&](auto &&fn) {
-    if (RC > 0) {
-#pragma unroll
-      for (int k = 0; k < (RC > 0 ? RC : 1); ++k) {
-        const int64_t gi = t + (int64_t)kEvictThreads * k;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int64_t i = 4 * gi + j;
-          if (i < n) fn(i, R.v[k][j]);
-        }
-      }
-    } else {
-      uint32_t dummy = 0;
-      for (int64_t gi = t; gi < ngroups; gi += kEvictThreads) {
-        float s[4];
-        load_group<RC>(sc, n, gi, s, dummy);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int64_t i = 4 * gi + j;
-          if (i < n) fn(i, s[j]);
-        }
-      }
+    for (int j = 0; j < 4; ++j) {
+      const int64_t i = 4 * gi + j;
+      const float c = clean_score(v[j], bad);
+      v[j] = (i < n && i >= tail_lo && i < tail_hi) ? c : -1.0f;
     }
+    return make_float4(v[0], v[1], v[2], v[3]);
+  };
+  auto group = [&](int64_t gi) -> float4 {
+    if (staged) return reinterpret_cast<const float4 *>(s_sc)[gi];
+    uint32_t dummy = 0;
+    return tail4(gi, load_raw(gi), dummy);
   };
 
-  // Tail statistics: |T|, #positive, sum_T s, max s, min positive s; bad-score flag.
+  // Pass 0: read (and stage) the scores; tail statistics; bad-score flag.  Four groups per
+  // thread are loaded before any is used so their latencies overlap.
+  uint32_t bad = 0;
   double n_tail = 0.0, n_pos = 0.0, s_sum = 0.0;
   float s_max = 0.0f, s_minp = INFINITY;
-  for_tokens([&](int64_t i, float s) {
-    if (in_tail(i, n, L.n_sink, L.n_recent)) {
-      n_tail += 1.0;
-      s_sum += (double)s;
-      if (s > 0.0f) {
-        n_pos += 1.0;
-        s_minp = fminf(s_minp, s);
+  for (int64_t g0 = 0; g0 < ngroups; g0 += kSelectThreads * 4) {
+    float4 raw[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) raw[q] = load_raw(g0 + kSelectThreads * q + t);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t gi = g0 + kSelectThreads * q + t;
+      if (gi >= ngroups) break;
+      // every position is checked for bad values, protected ones included
+      uint32_t b2 = 0;
+      const float4 tv = tail4(gi, raw[q], b2);
+      {
+        const float rv[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (4 * gi + j < n) clean_score(rv[j], bad);
       }
-      s_max = fmaxf(s_max, s);
-    }
-  });
-  if (RC == 0) {
-    // streamed path: the flag is raised while reading raw scores
-    for (int64_t i = t; i < n; i += kEvictThreads) {
-      const float s = sc[i];
-      if (!(s >= 0.0f) || isinf(s)) bad = 1u;
+      const float v[4] = {tv.x, tv.y, tv.z, tv.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (v[j] >= 0.0f) {
+          n_tail += 1.0;
+          s_sum += (double)v[j];
+          if (v[j] > 0.0f) {
+            n_pos += 1.0;
+            s_minp = fminf(s_minp, v[j]);
+          }
+          s_max = fmaxf(s_max, v[j]);
+        }
+      }
+      if (staged) reinterpret_cast<float4 *>(s_sc)[gi] = tv;
     }
   }
-  double badd = (double)bad;
-  block_sum3(n_tail, n_pos, s_sum, red3, b3);
-  block_minmax(s_max, s_minp, red2, b2);
+  block_sum3(n_tail, n_pos, s_sum, R, rbuf);
+  block_minmax(s_max, s_minp, R, rbuf);
   {
-    double z0 = badd, z1 = 0.0, z2 = 0.0;
-    block_sum3(z0, z1, z2, red3, b3);
-    badd = z0;
+    double b0 = (double)bad, z1 = 0.0, z2 = 0.0;
+    block_sum3(b0, z1, z2, R, rbuf);
+    bad = b0 > 0.0 ? 1u : 0u;
   }
+  uint32_t st = bad ? EBD_ST_BAD_SCORE : 0u;
 
-  uint32_t st = badd > 0.0 ? EBD_ST_BAD_SCORE : 0u;
   const double n_zero = n_tail - n_pos;
   double lam = 0.0;
   if (n_tail == 0.0) {
@@ -209,9 +205,9 @@ __global__ __launch_bounds__(kEvictThreads) void evict_solve_kernel(EvictLaunch 
     lam = INFINITY;
     st |= EBD_ST_NO_EVICTION;
   } else {
-    // g(lam) = H + eps L + lam S_mid is piecewise linear and nondecreasing.  Newton steps on the
-    // current piece (exact once the piece is right), safeguarded by a bracket [lo, hi] with
-    // g(lo) < m <= g(hi).
+    // g(lam) = H + eps L + lam S_mid is piecewise linear and nondecreasing.  A Newton step on
+    // the current piece is exact once the piece is right; the bracket [lo, hi] with
+    // g(lo) < m <= g(hi) guards every step.
     double lo = (double)eps / (double)s_max;
     double hi = 1.0 / (double)s_minp;
     double cur = fmin(fmax(m / s_sum, lo), hi);
@@ -219,57 +215,54 @@ __global__ __launch_bounds__(kEvictThreads) void evict_solve_kernel(EvictLaunch 
     bool from_newton = false;
     for (int it = 0; it < 96; ++it) {
       const float lf = (float)cur;
-      double H = 0.0, Lo = 0.0, S = 0.0;
-      for_tokens([&](int64_t i, float s) {
-        if (in_tail(i, n, L.n_sink, L.n_recent)) {
-          const float p = lf * s;
-          if (p >= 1.0f) H += 1.0;
-          else if (p <= eps) Lo += 1.0;
-          else S += (double)s;
+      float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
+      for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
+        const float4 s4 = group(gi);
+        const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float p = lf * sv[j];
+          const bool in = sv[j] >= 0.0f;
+          H += (in && p >= 1.0f) ? 1.0f : 0.0f;
+          Lo += (in && p <= eps) ? 1.0f : 0.0f;
+          Sm += (in && p > eps && p < 1.0f) ? sv[j] : 0.0f;
         }
-      });
-      block_sum3(H, Lo, S, red3, b3);
-      if (from_newton && H == pH && Lo == pL && S == pS) break;  // same piece: cur is exact
-      const double g = H + (double)eps * Lo + (double)lf * S;
+      }
+      double dH = H, dL = Lo, dS = Sm;
+      block_sum3(dH, dL, dS, R, rbuf);
+      if (from_newton && dH == pH && dL == pL && dS == pS) break;  // same piece: cur is exact
+      const double g = dH + (double)eps * dL + (double)lf * dS;
       if (g < m) lo = (double)lf;
       else hi = (double)lf;
       if (g == m) break;
-      double nxt = S > 0.0 ? (m - H - (double)eps * Lo) / S : -1.0;
+      double nxt = dS > 0.0 ? (m - dH - (double)eps * dL) / dS : -1.0;
       from_newton = (nxt > lo && nxt < hi);
       if (!from_newton) nxt = 0.5 * (lo + hi);
       if ((float)nxt == lf || hi - lo <= 1e-9 * hi) {
         cur = from_newton ? nxt : cur;
         break;
       }
-      pH = H;
-      pL = Lo;
-      pS = S;
+      pH = dH;
+      pL = dL;
+      pS = dS;
       cur = nxt;
     }
     lam = cur;
   }
   const float lamf = (float)lam;
 
-  // Retained count per chunk with the final pi: the same arithmetic evict_compact repeats.
-  const uint64_t sd = unit_seed(L, u);
-  const int64_t nch = (n + kEvictChunk - 1) / kEvictChunk;
-  double total = 0.0;
-  for (int64_t c = 0; c < nch; ++c) {
-    const int64_t gi = c * kEvictThreads + t;
-    double kept = 0.0;
-    if (4 * gi < n) {
-      float s[4];
-      uint32_t dummy = 0;
-      if (RC > 0) {
-#pragma unroll
-        for (int k = 0; k < (RC > 0 ? RC : 1); ++k)
-          if (k == c) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) s[j] = R.v[k][j];
-          }
-      } else {
-        load_group<RC>(sc, n, gi, s, dummy);
-      }
+  // Mask and in-order write of the retained rows' pi and positions: 1024-token blocks, ranks
+  // from per-wave ballots plus the counts of the lower waves.
+  const uint64_t sd = L.seed_per_unit ? L.seed_per_unit[u] : L.seed;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int64_t rank0 = 0;
+  for (int64_t g0 = 0; g0 < ngroups; g0 += kSelectThreads) {
+    const int64_t gi = g0 + t;
+    float p[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+    bool keep[4] = {false, false, false, false};
+    if (gi < ngroups) {
+      const float4 s4 = group(gi);
+      const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
       const uint4 x = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)u, L.epoch, kPhiloxTag),
                                     (uint32_t)sd, (uint32_t)(sd >> 32));
       const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
@@ -277,158 +270,107 @@ __global__ __launch_bounds__(kEvictThreads) void evict_solve_kernel(EvictLaunch 
       for (int j = 0; j < 4; ++j) {
         const int64_t i = 4 * gi + j;
         if (i < n) {
-          const float p = token_pi(in_tail(i, n, L.n_sink, L.n_recent), s[j], lamf, eps);
-          kept += keep_token(xw[j], p) ? 1.0 : 0.0;
+          p[j] = token_pi(sv[j] >= 0.0f, sv[j], lamf, eps);
+          keep[j] = keep_token(xw[j], p[j]);
+          if (L.pi_full) L.pi_full[base + i] = p[j];
         }
       }
     }
-    double z1 = 0.0, z2 = 0.0;
-    block_sum3(kept, z1, z2, red3, b3);
-    if (t == 0) L.ws_chunk_off[(int64_t)u * L.nchunk + c] = (int32_t)total;
-    total += kept;
+    int before = 0, wtot = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint64_t bal = __ballot(keep[j]);
+      before += __popcll(bal & below);
+      wtot += __popcll(bal);
+    }
+    if (lane == 0) s_tot[rbuf][wv] = wtot;
+    __syncthreads();
+    int wpre = 0, btot = 0;
+#pragma unroll
+    for (int w = 0; w < kSelectThreads / 64; ++w) {
+      const int c = s_tot[rbuf][w];
+      wpre += w < wv ? c : 0;
+      btot += c;
+    }
+    rbuf ^= 1;
+    int64_t r = rank0 + wpre + before;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (keep[j]) {
+        if (r < cap) {
+          L.pic[cbase + r] = p[j];
+          L.idxc[cbase + r] = (int32_t)(4 * gi + j);
+        }
+        ++r;
+      }
+    }
+    rank0 += btot;
   }
   if (t == 0) {
-    if ((int64_t)total > cap) st |= EBD_ST_CAP_OVERFLOW;
-    L.count[u] = (int32_t)total;
+    if (rank0 > cap) st |= EBD_ST_CAP_OVERFLOW;
+    L.count[u] = (int32_t)rank0;
     L.status[u] = st;
-    L.ws_lambda[u] = lamf;
     if (L.lambda_out) L.lambda_out[u] = lamf;
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// evict_compact: mask, rank, stable copy of retained rows
+// evict_copy: gather the retained K and V rows in order
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kEvictThreads) void evict_compact_kernel(EvictLaunch L) {
-  __shared__ int wave_tot[kEvictThreads / 64];
-  __shared__ uint16_t list[kEvictChunk];
+__global__ __launch_bounds__(kCopyThreads) void evict_copy_kernel(EvictLaunch L) {
   const int64_t bid = blockIdx.x;
-  const int c = (int)(bid % L.nchunk);
-  const int u = (int)(bid / L.nchunk);
-  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-  const int64_t base = L.seq_off[u];
-  const int64_t n = L.seq_off[u + 1] - base;
-  if ((int64_t)c * kEvictChunk >= n) return;
-  if ((n + kEvictChunk - 1) / kEvictChunk > (int64_t)L.nchunk) return;  // flagged by evict_solve
+  const int blk = (int)(bid % L.copy_blocks);
+  const int u = (int)(bid / L.copy_blocks);
   const int64_t cbase = L.cap_off[u];
   const int64_t cap = L.cap_off[u + 1] - cbase;
-  const float lamf = L.ws_lambda[u];
-  const float eps = L.pi_min;
-  const uint64_t sd = unit_seed(L, u);
-
-  const int64_t gi = (int64_t)c * kEvictThreads + t;
-  float p[4] = {1.0f, 1.0f, 1.0f, 1.0f};
-  uint32_t keep = 0;
-  if (4 * gi < n) {
-    uint32_t dummy = 0;
-    float s[4];
+  const int64_t nkeep = min((int64_t)L.count[u], cap);
+  const int64_t r0 = (int64_t)blk * kCopyRows;
+  if (r0 >= nkeep || (L.seq_off[u + 1] - L.seq_off[u]) > L.max_rows) return;
+  const int64_t base = L.seq_off[u];
+  const int sub = threadIdx.x & 15;
+  const int row = threadIdx.x >> 4;
+  constexpr int kPass = kCopyThreads / 16;  // rows per pass
+  constexpr int kIter = kCopyRows / kPass;  // passes per block
+  const u32x4 *K4 = reinterpret_cast<const u32x4 *>(L.K);
+  const u32x4 *V4 = reinterpret_cast<const u32x4 *>(L.V);
+  u32x4 *Kc4 = reinterpret_cast<u32x4 *>(L.Kc);
+  u32x4 *Vc4 = reinterpret_cast<u32x4 *>(L.Vc);
+  // Rows past the end load a valid row (the block's first) and skip the store, so every load
+  // is unconditional and all of a thread's loads are in flight together.
+  int32_t src[kIter];
+  bool ok[kIter];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t i = 4 * gi + j;
-      s[j] = i < n ? clean_score(L.scores[base + i], dummy) : 0.0f;
-    }
-    const uint4 x = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)u, L.epoch, kPhiloxTag),
-                                  (uint32_t)sd, (uint32_t)(sd >> 32));
-    const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t i = 4 * gi + j;
-      if (i < n) {
-        p[j] = token_pi(in_tail(i, n, L.n_sink, L.n_recent), s[j], lamf, eps);
-        if (keep_token(xw[j], p[j])) keep |= 1u << j;
-        if (L.pi_full) L.pi_full[base + i] = p[j];
-      }
-    }
+  for (int k = 0; k < kIter; ++k) {
+    const int64_t r = r0 + row + k * kPass;
+    ok[k] = r < nkeep;
+    src[k] = L.idxc[cbase + (ok[k] ? r : r0)];
   }
-  // Block exclusive scan of the per-thread retained counts.
-  const int cnt = __popc(keep);
-  int incl = cnt;
+  u32x4 kv[kIter], vv[kIter];
 #pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int y = __shfl_up(incl, d);
-    if (lane >= d) incl += y;
+  for (int k = 0; k < kIter; ++k) {
+    const int64_t s = (base + src[k]) * (kHeadDim / 8) + sub;
+    kv[k] = K4[s];
+    vv[k] = V4[s];
   }
-  if (lane == 63) wave_tot[wv] = incl;
-  __syncthreads();
-  int wpre = 0, nret = 0;
 #pragma unroll
-  for (int w = 0; w < kEvictThreads / 64; ++w) {
-    const int v = wave_tot[w];
-    wpre += w < wv ? v : 0;
-    nret += v;
-  }
-  const int64_t chunk_off = L.ws_chunk_off[(int64_t)u * L.nchunk + c];
-  int r = wpre + incl - cnt;  // rank within the chunk
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (keep & (1u << j)) {
-      const int64_t g = chunk_off + r;
-      if (g < cap) {
-        L.pic[cbase + g] = p[j];
-        L.idxc[cbase + g] = (int32_t)(4 * gi + j);
-      }
-      list[r] = (uint16_t)(4 * t + j);
-      ++r;
-    }
-  }
-  __syncthreads();
-
-  // Copy the retained rows: 16 lanes per 256-byte row, 32 rows per pass, 4 passes in flight.
-  const int sub = t & 15;
-  const int row0 = t >> 4;
-  const int64_t cbeg = (int64_t)c * kEvictChunk;
-  const int64_t room = cap - chunk_off;  // rows of this chunk that still fit
-  const int nrow = (int)min((int64_t)nret, max(room, (int64_t)0));
-  const uint4 *K4 = reinterpret_cast<const uint4 *>(L.K);
-  const uint4 *V4 = reinterpret_cast<const uint4 *>(L.V);
-  uint4 *Kc4 = reinterpret_cast<uint4 *>(L.Kc);
-  uint4 *Vc4 = reinterpret_cast<uint4 *>(L.Vc);
-  constexpr int kRowsPerPass = kEvictThreads / 16;
-  for (int rr = row0; rr < nrow; rr += 4 * kRowsPerPass) {
-    uint4 kv[4], vv[4];
-    int64_t dst[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int ro = rr + q * kRowsPerPass;
-      dst[q] = -1;
-      if (ro < nrow) {
-        const int64_t src = (base + cbeg + list[ro]) * (kHeadDim / 8) + sub;
-        kv[q] = K4[src];
-        vv[q] = V4[src];
-        dst[q] = (cbase + chunk_off + ro) * (kHeadDim / 8) + sub;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (dst[q] >= 0) {
-        Kc4[dst[q]] = kv[q];
-        Vc4[dst[q]] = vv[q];
-      }
+  for (int k = 0; k < kIter; ++k) {
+    if (ok[k]) {
+      const int64_t d = (cbase + r0 + row + k * kPass) * (kHeadDim / 8) + sub;
+      Kc4[d] = kv[k];
+      Vc4[d] = vv[k];
     }
   }
 }
 
-size_t evict_workspace_bytes(int32_t U, int32_t nchunk) {
-  const size_t a = ((size_t)U * sizeof(float) + 255) & ~(size_t)255;
-  const size_t b = ((size_t)U * (size_t)nchunk * sizeof(int32_t) + 255) & ~(size_t)255;
-  return a + b;
-}
-
-hipError_t launch_evict_solve(const EvictLaunch &L, hipStream_t s) {
-  const dim3 grid(L.U), block(kEvictThreads);
-  switch (L.reg_chunks) {
-    case 1: hipLaunchKernelGGL(evict_solve_kernel<1>, grid, block, 0, s, L); break;
-    case 2: hipLaunchKernelGGL(evict_solve_kernel<2>, grid, block, 0, s, L); break;
-    case 4: hipLaunchKernelGGL(evict_solve_kernel<4>, grid, block, 0, s, L); break;
-    case 8: hipLaunchKernelGGL(evict_solve_kernel<8>, grid, block, 0, s, L); break;
-    default: hipLaunchKernelGGL(evict_solve_kernel<0>, grid, block, 0, s, L); break;
-  }
+hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s) {
+  const size_t lds = L.stage_rows > 0 ? (size_t)((L.stage_rows + 3) / 4) * 16 : 0;
+  hipLaunchKernelGGL(evict_select_kernel, dim3(L.U), dim3(kSelectThreads), lds, s, L);
   return hipGetLastError();
 }
 
-hipError_t launch_evict_compact(const EvictLaunch &L, hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)L.U * L.nchunk)), block(kEvictThreads);
-  hipLaunchKernelGGL(evict_compact_kernel, grid, block, 0, s, L);
+hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s) {
+  const dim3 grid((unsigned)((int64_t)L.U * L.copy_blocks)), block(kCopyThreads);
+  hipLaunchKernelGGL(evict_copy_kernel, grid, block, 0, s, L);
   return hipGetLastError();
 }
 

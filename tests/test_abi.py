@@ -56,6 +56,7 @@ def _evict_params(ebd, **kw):
     p.num_units = kw.get("U", 4)
     p.head_dim = kw.get("d", 128)
     p.max_rows = kw.get("max_rows", 4096)
+    p.max_capacity = kw.get("max_capacity", 1024)
     p.seq_off = FAKE
     p.cap_off = FAKE
     p.n_sink, p.n_recent = 4, 64
@@ -82,6 +83,7 @@ def test_evict_argument_validation():
     assert _call_evict(lib, _evict_params(ebd, U=-1)) == ebd.EBD_ERR_INVALID_ARG
     assert _call_evict(lib, _evict_params(ebd), nulls=(0,)) == ebd.EBD_ERR_INVALID_ARG
     assert _call_evict(lib, _evict_params(ebd), ws_bytes=16) == ebd.EBD_ERR_WORKSPACE
+    assert _call_evict(lib, _evict_params(ebd, max_capacity=-1)) == ebd.EBD_ERR_INVALID_ARG
     assert _call_evict(lib, _evict_params(ebd), ws=FAKE + 8) == ebd.EBD_ERR_WORKSPACE
     assert _call_evict(lib, _evict_params(ebd), ws=None) == ebd.EBD_ERR_WORKSPACE
     # misaligned K
@@ -123,8 +125,7 @@ def test_workspace_sizes():
     ebd, lib = _lib()
     p = _evict_params(ebd, U=1792, max_rows=6144)
     n = ebd.ebd_workspace_size(ebd.EBD_WS_EVICT, p)
-    # lambda per unit + chunk offsets (3 chunks of 2048 per unit), each region 256-aligned
-    assert n == ((1792 * 4 + 255) // 256) * 256 + ((1792 * 3 * 4 + 255) // 256) * 256
+    assert n == 256  # reserved: the sampler's launches share only the index list they write
     a = ebd.ebd_attend_params()
     a.num_units, a.group, a.head_dim, a.max_rows, a.cap_off = 1792, 7, 128, 1856, FAKE
     a.delta = 0.1
