@@ -55,6 +55,57 @@ def load_traffic(workload: str, kernel: str):
     return None if k is None else k.get("bytes_per_launch")
 
 
+def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str) -> int:
+    """Per-launch HBM bytes of the library's kernels from two rocprofv3 --pmc csv runs.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same counter reads
+    for the 1 GiB device copy that --copy-calibration runs (1 GiB read, 1 GiB written).
+    Writes profiles/hbm_traffic_<workload>.json (read by the benchmark while the kernel sources
+    are unchanged) and a short text summary next to it.
+    """
+    import csv
+    import glob
+    import statistics
+
+    def load(d, counter):
+        per, calib = {}, []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for row in csv.DictReader(open(f)):
+                if row["Counter_Name"] != counter:
+                    continue
+                name, v = row["Kernel_Name"], float(row["Counter_Value"])
+                if "ebd::" in name:
+                    k = name.split("(")[0].replace("void ", "").replace("ebd::", "")
+                    k = k.replace("_kernel", "").split("<")[0]
+                    per.setdefault(k, []).append(v)
+                elif "copyBuffer" in name and v > 0.25 * (1 << 20):
+                    calib.append(v)  # the 1 GiB calibration copies
+        return per, calib
+
+    fetch, fcal = load(fetch_dir, "FETCH_SIZE")
+    write, wcal = load(write_dir, "WRITE_SIZE")
+    if not fcal or not wcal:
+        print("no calibration copy found in the counter runs", file=sys.stderr)
+        return 1
+    gib_kib = float(1 << 20)
+    fscale = gib_kib / statistics.median(fcal)  # true KiB per counted KiB
+    wscale = gib_kib / statistics.median(wcal)
+    kernels = {}
+    for k in sorted(set(fetch) | set(write)):
+        fb = statistics.mean(fetch.get(k, [0.0])) * fscale * 1024
+        wb = statistics.mean(write.get(k, [0.0])) * wscale * 1024
+        kernels[k] = {"fetch_bytes_per_launch": int(fb), "write_bytes_per_launch": int(wb),
+                      "bytes_per_launch": int(fb + wb),
+                      "launches_profiled": len(fetch.get(k, []))}
+    rec = {"workload": workload, "kernel_sources_hash": kernel_sources_hash(),
+           "fetch_scale": fscale, "write_scale": wscale, "kernels": kernels, "command": command}
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % workload)
+    json.dump(rec, open(path, "w"), indent=1)
+    print(json.dumps(rec, indent=1))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -67,7 +118,14 @@ def main() -> int:
                     help="after timing, run a plain 1 GiB device copy (profiler counter scale)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate host time for the oracle baseline (0 disables it)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/hbm_traffic_<workload>.json from rocprofv3 --pmc csv runs")
+    ap.add_argument("--pmc-command", default="", help="command recorded in the summary")
     args = ap.parse_args()
+
+    if args.summarize_pmc:
+        return summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload,
+                             args.pmc_command)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -130,7 +130,7 @@ def test_workspace_sizes():
     a.num_units, a.group, a.head_dim, a.max_rows, a.cap_off = 1792, 7, 128, 1856, FAKE
     a.delta = 0.1
     m = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a)
-    assert m == 256 + 1792 * 2 * 7 * 288 * 4  # two splits of 1024 rows
+    assert m == 256 + 1792 * 2 * 7 * 328 * 4  # two splits of 1024 rows, 328-float records
     assert lib.ebd_workspace_size(7, ctypes.byref(a)) == 0
 
 
