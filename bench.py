@@ -171,11 +171,13 @@ def main() -> int:
                               b, None, wl.pi_min, 0, args.seed, None, 0)
         ews = ebd.workspace(ebd.ebd_workspace_size(ebd.EBD_WS_EVICT, ep))
         ap_ = ebd.attend_params(U, G, rc.max_cap, cap_off)
-        aws = ebd.workspace(ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, ap_))
+        aws_bytes = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, ap_)
+        aws = ebd.workspace(aws_bytes)
         out = {k: torch.empty(s, dtype=torch.float32, device="cuda")
                for k, s in (("y", (U, G, 128)), ("vhat", (U, G)), ("lse", (U, G)),
                             ("b", (U, G)), ("r", (U, G)))}
-        plans.append(dict(budget=b, rc=rc, ep=ep, ews=ews, ap=ap_, aws=aws, out=out))
+        plans.append(dict(budget=b, rc=rc, ep=ep, ews=ews, ap=ap_, aws=aws, out=out,
+                          fused=cache.fused_finalize(aws_bytes, U, G)))
 
     def step():
         for p in plans:
@@ -214,23 +216,25 @@ def main() -> int:
     retained_total = 0
     for p in plans:
         cnt = p["rc"].count.cpu().numpy().astype(np.int64)
-        rescans = cache.rescans(p["aws"])
+        rescans = cache.rescans(p["aws"], U, G)
         per_budget.append(dict(budget=p["budget"], retained_rows=int(cnt.sum()),
                                mean_retained_per_unit=float(cnt.mean()),
-                               range_term_rescans=int(rescans)))
+                               range_term_rescans=int(rescans), fused_finalize=bool(p["fused"])))
         retained_total += int(cnt.sum())
     K = args.steps
     nb = len(plans)
     kv_bytes = 512 * retained_total  # K + V bf16 rows retained, per step (all budgets)
+    nfused = sum(1 for p in plans if p["fused"])
     alg = {
         # scores read once per cached token; pi and index written per retained row
         "evict_select": 4 * U * n * nb + 8 * retained_total,
         # read K+V rows (512 B) and write Kc+Vc rows (512 B) per retained row
         "evict_copy": 1024 * retained_total,
-        # K, V, pi per retained row (516 B) and the query heads
-        "attend_split": 516 * retained_total + nb * U * G * 256,
-        # y (512 B), vhat, lse, b, r per query head
-        "attend_finalize": nb * U * G * (512 + 16),
+        # K, V, pi per retained row (516 B) and the query heads; a split kernel that finalizes
+        # its units itself also writes y (512 B), vhat, lse, b, r per query head
+        "attend_split": 516 * retained_total + nb * U * G * 256 + nfused * U * G * (512 + 16),
+        # y, vhat, lse, b, r per query head of budgets whose units span several splits
+        "attend_finalize": (nb - nfused) * U * G * (512 + 16),
     }
     kern = {}
     for k in KERNELS:

@@ -120,8 +120,8 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
  *   max_rows host value >= max_u (cap_off[u+1] - cap_off[u]); sizes the split grid.
  *   scale: logit scale (0 means 1/sqrt(head_dim)); delta (0 means 0.1) and eps0
  *   (0 means 1e-9): the confidence level and normaliser of eq. (4).
- *   split_rows: retained rows per work-group split (0 = library choice; else a multiple
- *   of 64 in [64, 65536]).  Retained rows of a unit beyond max_rows are ignored.
+ *   split_rows: retained rows per split, one wave each (0 = library choice; else a
+ *   multiple of 16 in [16, 8192]).  Retained rows of a unit beyond max_rows are ignored.
  *   flags: reserved, must be 0.
  */
 typedef struct ebd_attend_params {
@@ -147,7 +147,11 @@ typedef struct ebd_attend_params {
  *     lse    [U, G]       ln Nhat, Nhat = sum_S a/pi (a = exp(scale q.k)); -inf if S empty
  *     brange [U, G]       range term b of eq. (4) (exact maximum), or NULL
  *     radius [U, G]       radius r of eq. (4), or NULL
- *   workspace: at least ebd_workspace_size(EBD_WS_ATTEND, p) bytes, 256-byte aligned.
+ *   workspace: at least ebd_workspace_size(EBD_WS_ATTEND, p) bytes, 256-byte aligned; y must
+ *   be 16-byte aligned.  After the call the workspace starts with U * ceil(G / 8) uint32
+ *   counts, per (unit, block of 8 query heads): the 512-row chunks re-read to make the range
+ *   term exact (0 when the kept candidates already decide it).  When every unit fits one
+ *   split, the whole step is one kernel and the workspace holds only these counts.
  */
 ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
                               const uint16_t *Vc, const float *pic, const int32_t *count,

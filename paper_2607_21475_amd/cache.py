@@ -117,6 +117,15 @@ def attend_certify(cache: RetainedCache, q: torch.Tensor, split_rows: int = 0, d
     return {"y": y, "vhat": vhat, "lse": lse, "b": b, "r": r, "ws": ws}
 
 
-def rescans(ws: torch.Tensor) -> int:
-    """Split rescans the last ebd_attend_certify on `ws` needed for the exact range term."""
-    return int(ws[:4].view(torch.int32)[0].item())
+def rescans(ws: torch.Tensor, num_units: int, group: int) -> int:
+    """512-row chunks the last ebd_attend_certify on `ws` rescanned for the exact range term
+    (the workspace starts with one count per unit and block of 8 query heads)."""
+    nhb = (int(group) + 7) // 8
+    return int(ws[: 4 * num_units * nhb].view(torch.int32).sum().item())
+
+
+def fused_finalize(ws_bytes: int, num_units: int, group: int) -> bool:
+    """Whether an attention launch planned with this workspace size finalizes inside its split
+    kernel (every unit is one split: the workspace holds only the rescan counts)."""
+    nhb = (int(group) + 7) // 8
+    return ws_bytes <= (4 * num_units * nhb + 255) // 256 * 256

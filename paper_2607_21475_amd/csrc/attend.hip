@@ -10,17 +10,18 @@
 //     C2 = sum c |v|^2 (the 2^{-2m} factors cancel against (sum w)^2)
 //   b = max_j sqrt(1 - pi_j) w_j |v_j - yhat| / sum w  (exact: candidates + bound check)
 //
-// attend_split (one work-group of four waves per (unit, split of the retained rows)):
-//   Each wave walks 16-row tiles with the next tile's loads in flight while the current one is
-//   computed.  q.k runs on MFMA (16x16x32 bf16, exact products, fp32 sums): A = K tile (16 rows x
-//   32 dims per k-block, loaded straight from HBM in operand layout), B = [q_0 .. q_{GB-1},
-//   q_0 .. q_{GB-1}, 0 ..] (16 columns).  Each lane then holds 4 rows x 1 column of logits;
-//   columns < GB become weights w, columns GB..2GB-1 (same logits) become variance weights c.
-//   f32 16x16x4 MFMAs then form o = sum w v (rows < GB) and Cv = sum c v (rows GB..2GB-1)
-//   together, with V in its natural row-major layout (no transpose, exact fp32 products).
+// attend_split (one wave per (unit, split of the retained rows, block of <= 8 query heads)):
+//   The wave walks its split in 16-row tiles with two tiles' loads in flight while a third is
+//   computed (raw buffer loads bounded by the split, so tail rows read as zero).  q.k runs on
+//   MFMA (16x16x32 bf16, exact products, fp32 sums): A = K tile (16 rows x 32 dims per k-block,
+//   loaded straight from HBM in operand layout), B = [q_0 .. q_{GB-1}, q_0 .. q_{GB-1}, 0 ..]
+//   (16 columns).  Each lane then holds 4 rows x 1 column of logits; columns < GB become weights
+//   w, columns GB..2GB-1 (same logits) become variance weights c.  f32 16x16x4 MFMAs then form
+//   o = sum w v (rows < GB) and Cv = sum c v (rows GB..2GB-1) together, with V in its natural
+//   row-major layout (no transpose, exact fp32 products).
 //   Range-term candidates: every weight lane keeps its four largest g^2 |v|^2 (g^2 = (1 - pi) w^2)
-//   among its rows, plus the maxima of g^2 |v|^2 and of g^2 over what it dropped; the
-//   work-group stores the 32 largest per head, their largest |v| and the non-candidate maxima.
+//   among its rows, plus the maxima of g^2 |v|^2 and of g^2 over what it dropped; the split's
+//   record holds those 16 candidates per head, their largest |v| and the non-candidate maxima.
 //   The running max m moves lazily (only by jumps of more than 2^8 in weight).
 // attend_finalize (one wave per (unit, query head)): log-sum-exp combine of the split records,
 //   yhat, Vhat, ln Nhat, the exact range term b (only candidates whose bound can still win are
@@ -45,24 +46,42 @@ __device__ __forceinline__ float scale_of(float mw, float M) {
   return (mw == -INFINITY) ? 0.0f : fast_exp2(mw - M);
 }
 
+// Upper bound of a finite x >= 0 in bf16 (round toward +inf), as the high 16 bits.
+__device__ __forceinline__ uint32_t bf16_up(float x) {
+  const uint32_t b = __float_as_uint(x);
+  return (b >> 16) + ((b & 0xffffu) ? 1u : 0u);
+}
+
+// Buffer resources (gfx9 raw buffers: stride 0, range checked per access).  Loads at or beyond
+// the range return zeros without touching memory, so a split's tail tiles and the prefetches past
+// its end need no clamping.
+constexpr int kRsrcWord3 = 0x00020000;  // 32-bit data format, untyped access
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)nbytes,
+                                           kRsrcWord3);
+}
+
 struct Tile {
-  uint4 k[4];  // K rows rb + c, dims 32 kb + 8 g .. + 7 (A operand of q.k)
-  uint4 v[4];  // V rows rb + 4 g + j, dims 8 c .. 8 c + 7 (B operand of the weighted sums)
-  float p[4];  // pi of rows rb + 4 g + j
+  u32x4 k[4];  // K rows 16t + c, dims 32 kb + 8 g .. + 7 (A operand of q.k)
+  u32x4 v[4];  // V rows 16t + 4 g + j, dims 8 c .. 8 c + 7 (B operand of the weighted sums)
+  float p[4];  // pi of rows 16t + 4 g + j
 };
 
-// Row offsets are unsigned 32-bit (a unit's region is < 2^31 rows), so the loads use a uniform
-// base plus a 32-bit lane offset.
-__device__ __forceinline__ void load_tile(Tile &T, const uint4 *Kb, const uint4 *Vb,
-                                          const float *Pb, int rb, int rlast, int g, int c) {
-  const uint32_t rk = (uint32_t)min(rb + c, rlast);
+// Tile t of a split (rows 16t .. 16t + 15 counted from the split's first row).
+__device__ __forceinline__ void load_tile(Tile &T, __amdgpu_buffer_rsrc_t rK, __amdgpu_buffer_rsrc_t rV,
+                                          __amdgpu_buffer_rsrc_t rP, int t, int g, int c) {
+  const uint32_t rk = (uint32_t)(16 * t + c);
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) T.k[kb] = Kb[rk * (kHeadDim / 8) + (uint32_t)(4 * kb + g)];
+  for (int kb = 0; kb < 4; ++kb)
+    T.k[kb] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            rK, rk * 256u + (uint32_t)(64 * kb + 16 * g), 0, 0));
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const uint32_t r = (uint32_t)min(rb + 4 * g + j, rlast);
-    T.v[j] = Vb[r * (kHeadDim / 8) + (uint32_t)c];
-    T.p[j] = Pb[r];
+    const uint32_t r = (uint32_t)(16 * t + 4 * g + j);
+    T.v[j] = __builtin_bit_cast(u32x4,
+                                __builtin_amdgcn_raw_buffer_load_b128(rV, r * 256u + 16u * c, 0, 0));
+    T.p[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rP, r * 4u, 0, 0));
   }
 }
 
@@ -71,7 +90,6 @@ struct SplitState {
   float mrun, s0, s1;
   float ck[4], cg[4], dk, dg;  // candidate lists (descending g^2 |v|^2, with g^2) and dropped maxima
   int cr[4];
-  int rowbase;                 // row of this lane's first logit in the current tile
 };
 
 // The running max moves only when a logit exceeds it by more than kLazy (log2 units): weights then
@@ -79,8 +97,11 @@ struct SplitState {
 // cross-lane max.
 constexpr float kLazy = 8.0f;
 
+// One 16-row tile: rows 16t + 4g + i of the split for this lane's head slot; `nvalid` rows of the
+// lane's row group are real (<= 0 masks them all), `rowbase` is the unit row of its first one.
 __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const bf16x8 (&qop)[4],
-                                           int nvalid, int g, bool isC, float scale2) {
+                                           int nvalid, int rowbase, bool isC, bool mine,
+                                           float scale2) {
   f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
@@ -95,7 +116,6 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
   lp[1] = dpp_f<0x55>(lq);  // quad_perm [1,1,1,1]
   lp[2] = dpp_f<0xAA>(lq);  // quad_perm [2,2,2,2]
   lp[3] = dpp_f<0xFF>(lq);  // quad_perm [3,3,3,3]
-  // lane (g, c): base-2 logits of rows rb + 4g + i for head slot c (nvalid <= 0 masks all)
   float lg[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) lg[i] = i < nvalid ? fmaf(sacc[i], scale2, -lp[i]) : -INFINITY;
@@ -106,9 +126,9 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
     const float mnew = fmaxf(S.mrun, tmax);
     const float alpha = (mnew > S.mrun) ? fast_exp2(S.mrun - mnew) : 1.0f;
     const float as = isC ? alpha * alpha : alpha;  // variance terms carry 2^{-2m}
-    const float a2 = alpha * alpha;               // candidate keys are squares
+    const float a2 = alpha * alpha;               // candidate keys and C2 are squares
     S.s0 *= as;
-    S.s1 *= as;
+    S.s1 *= a2;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       S.ck[e] *= a2;
@@ -118,7 +138,7 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
     S.dg *= a2;
     float ai[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ai[i] = __shfl(as, 4 * (__lane_id() >> 4) + i);  // row 4g + i
+    for (int i = 0; i < 4; ++i) ai[i] = __shfl(as, 4 * (__lane_id() >> 4) + i);  // slot 4g + i
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
 #pragma unroll
@@ -130,7 +150,7 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
   float vf[4][8], nv2[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const uint32_t w4[4] = {T.v[j].x, T.v[j].y, T.v[j].z, T.v[j].w};
+    const uint32_t w4[4] = {T.v[j][0], T.v[j][1], T.v[j][2], T.v[j][3]};
     float sq = 0.0f;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -162,12 +182,13 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
       S.acc[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(val[j], vf[j][db], S.acc[db], 0, 0, 0);
   }
 
-  // Range-term candidates: every row of the tile is offered to the lane's sorted top-4; whatever
-  // falls off the end only raises the dropped maxima.
+  // Range-term candidates: weight lanes take the rows of even tiles, variance lanes (same
+  // logits) those of odd tiles (`mine`).  Every such row is offered to the lane's sorted top-4;
+  // whatever falls off the end only raises the dropped maxima.
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    float nk = kap[i], ng = gsq[i];
-    int nr = S.rowbase + i;
+    float nk = mine ? kap[i] : 0.0f, ng = mine ? gsq[i] : 0.0f;
+    int nr = rowbase + i;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bool sw = nk > S.ck[e];
@@ -185,30 +206,390 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
   }
 }
 
+// End of a chunk: the lane lists of head h (weight lanes (g, h), variance lanes (g, GB + h))
+// become the chunk's 32 candidates in LDS, with the chunk's dropped maxima and the running max
+// they are scaled by; the lists restart empty for the next chunk.  `c0` is the chunk's first
+// unit row.
+template <int GB>
+__device__ __forceinline__ void flush_chunk(SplitState &S, float *s_chunk, int k, int g, int c,
+                                            int c0) {
+  float dk = S.dk, dg = S.dg, vm = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) vm = fmaxf(vm, S.cg[e] > 0.0f ? S.ck[e] / S.cg[e] : 0.0f);
+  const float al = fast_sqrt(dk);              // this lane's own dropped maximum of g |v|
+  const float ao = __shfl_xor(al, 16);         // ... and that of row group g ^ 1
+  dk = fmaxf(dk, __shfl_xor(dk, 16));
+  dk = fmaxf(dk, __shfl_xor(dk, 32));
+  dg = fmaxf(dg, __shfl_xor(dg, 16));
+  dg = fmaxf(dg, __shfl_xor(dg, 32));
+  vm = fmaxf(vm, __shfl_xor(vm, 16));
+  vm = fmaxf(vm, __shfl_xor(vm, 32));
+  const int lane = __lane_id();
+  const int partner = (lane + GB) & 63;  // the variance lane of the same head and row group
+  dk = fmaxf(dk, __shfl(dk, partner));
+  dg = fmaxf(dg, __shfl(dg, partner));
+  vm = fmaxf(vm, __shfl(vm, partner));
+  if (c < 2 * GB) {
+    const int h = c < GB ? c : c - GB;
+    const int j0 = (c < GB ? 0 : 16) + 4 * g;
+    float *blk = s_chunk + (k * GB + h) * kChunkFloats;
+    uint32_t off[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool real = S.cr[e] >= 0 && S.ck[e] > 0.0f;
+      blk[kChG + j0 + e] = real ? fast_sqrt(S.cg[e]) : 0.0f;
+      off[e] = real ? (uint32_t)(S.cr[e] - c0) : 0u;
+    }
+    blk[kChI + j0 / 2] = __uint_as_float(off[0] | (off[1] << 16));
+    blk[kChI + j0 / 2 + 1] = __uint_as_float(off[2] | (off[3] << 16));
+    if ((g & 1) == 0)  // lanes 4w + g and 4w + g + 1 (w = 0 weight, 1 variance lanes)
+      blk[kChAL + g / 2 + (c < GB ? 0 : 2)] = __uint_as_float(bf16_up(al) | (bf16_up(ao) << 16));
+    if (c < GB && g == 0) {
+      blk[kChA] = fast_sqrt(dk);
+      blk[kChB] = fast_sqrt(dg);
+      blk[kChVmax] = fast_sqrt(vm);
+      blk[kChM] = S.mrun;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    S.ck[e] = S.cg[e] = 0.0f;
+    S.cr[e] = -1;
+  }
+  S.dk = S.dg = 0.0f;
+}
+
 }  // namespace
 
-template <int GB>
-__global__ __launch_bounds__(kAttendThreads, 2) void attend_split_kernel(AttendLaunch L, int h0) {
-  __shared__ float s_acc[4][16][kHeadDim];
-  __shared__ float s_m[4][16], s_s0[4][16], s_s1[4][16];
-  __shared__ float s_ck[GB][64], s_cg[GB][64];
-  __shared__ int s_cr[GB][64];
-  __shared__ float s_dk[GB][16], s_dg[GB][16];
-  __shared__ __align__(16) float s_key[4][64];
+// ---------------------------------------------------------------------------------------------
+// Finalize of a block of GB heads of one unit: yhat, Vhat, ln Nhat, the exact range term b and
+// the radius r, from the combined sums in LDS and the candidate blocks of every chunk.
+// ---------------------------------------------------------------------------------------------
+constexpr int kListCap = 256;  // candidates evaluated per batch
+constexpr int kHs = 8;         // per-head table: M, l, C0, C2, |yhat|, lb, Vhat, -
+constexpr int kHsM = 0, kHsL = 1, kHsC0 = 2, kHsC2 = 3, kHsYn = 4, kHsLb = 5, kHsV = 6;
 
+// LDS of the finalize, carved from one dynamic buffer.
+template <int GB>
+struct FinLds {
+  float *o;                  // [2 GB][128]: o, later yhat (slots < GB); Cv, later q (the rest)
+  float *hs;                 // [GB][kHs]
+  unsigned long long *best;  // [GB]: (bound bits << 32) | candidate index of the largest bound
+  int *list;                 // [kListCap]
+  __device__ explicit FinLds(float *base) {
+    o = base;
+    hs = o + 2 * GB * kHeadDim;
+    best = reinterpret_cast<unsigned long long *>(hs + GB * kHs);
+    list = reinterpret_cast<int *>(best + GB);
+  }
+  static constexpr size_t bytes() {
+    return (2 * GB * kHeadDim + GB * kHs) * sizeof(float) + GB * sizeof(unsigned long long) +
+           kListCap * sizeof(int);
+  }
+};
+
+// Where the candidate block of (split s, chunk k, head h) lives: LDS for a fused split, the
+// split records in the workspace otherwise.
+struct CandSrc {
+  const float *base;
+  int64_t sstride;
+  int kstride, hstride;
+};
+
+template <int GB>
+__device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, int64_t cbase,
+                               int nsp, const CandSrc &C, const FinLds<GB> &F) {
+  const int lane = threadIdx.x & 63;
+  const int64_t uh0 = (int64_t)u * L.G + h0;
+
+  // (1) yhat, Vhat, ln Nhat: 8 lanes per head, 16 dims per lane.
+  {
+    const int h = lane >> 3, j = lane & 7;
+    float yy = 0.0f, ycv = 0.0f;
+    if (h < GB) {
+      const float l = F.hs[h * kHs + kHsL];
+      float4 *oh = reinterpret_cast<float4 *>(F.o + h * kHeadDim + 16 * j);
+      const float4 *cv = reinterpret_cast<const float4 *>(F.o + (GB + h) * kHeadDim + 16 * j);
+      float4 *yo = reinterpret_cast<float4 *>(L.y + (uh0 + h) * kHeadDim + 16 * j);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 a = oh[q];
+        const float4 b = cv[q];
+        a.x /= l;
+        a.y /= l;
+        a.z /= l;
+        a.w /= l;
+        yy += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+        ycv += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+        oh[q] = a;
+        yo[q] = a;
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) {
+      yy += __shfl_xor(yy, o);
+      ycv += __shfl_xor(ycv, o);
+    }
+    if (h < GB && j == 0) {
+      float *hs = F.hs + h * kHs;
+      const float l = hs[kHsL];
+      const float V = fmaxf(hs[kHsC2] - 2.0f * ycv + yy * hs[kHsC0], 0.0f) / (l * l);
+      L.vhat[uh0 + h] = V;
+      L.lse[uh0 + h] = hs[kHsM] * kLn2 + logf(l);
+      hs[kHsYn] = sqrtf(yy);
+      hs[kHsLb] = 0.0f;
+      hs[kHsV] = V;
+      F.best[h] = 0ull;
+    }
+  }
+  __syncthreads();
+
+  // (2) Candidate bounds: a candidate's value f g |v - yhat| / l is at most f g (Vmax + |yhat|)/l.
+  //     Candidate e = ((s nchunk + k) GB + h) kCand + j.
+  const int R = L.split_rows;
+  const int E = nsp * L.nchunk * GB * kCand;
+  auto decode = [&](int e, int &h, int &row, float &fg, float &ub) -> bool {
+    const int j = e % kCand;
+    int r = e / kCand;
+    h = r % GB;
+    r /= GB;
+    const int k = r % L.nchunk, s = r / L.nchunk;
+    if (k * kChunkRows >= min(cnt - s * R, R)) return false;  // no such chunk
+    const float *blk = C.base + s * C.sstride + k * C.kstride + h * C.hstride;
+    const float gj = blk[kChG + j];
+    if (!(gj > 0.0f)) return false;
+    row = s * R + k * kChunkRows + (int)((__float_as_uint(blk[kChI + j / 2]) >> (16 * (j & 1))) & 0xffffu);
+    const float *hs = F.hs + h * kHs;
+    fg = scale_of(blk[kChM], hs[kHsM]) * gj / hs[kHsL];
+    ub = fg * (blk[kChVmax] + hs[kHsYn]);
+    return true;
+  };
+  for (int e = lane; e < E; e += 64) {
+    int h, row;
+    float fg, ub;
+    if (decode(e, h, row, fg, ub) && ub > 0.0f)
+      atomicMax(&F.best[h], ((unsigned long long)__float_as_uint(ub) << 32) | (unsigned)e);
+  }
+  __syncthreads();
+
+  // (3) The most promising candidate of every head, 8 lanes per head.
+  {
+    const int h = lane >> 3, j = lane & 7;
+    float d2 = 0.0f, fg = 0.0f;
+    bool have = false;
+    if (h < GB && F.best[h] != 0ull) {
+      int hh, row;
+      float ub;
+      have = decode((int)(F.best[h] & 0xffffffffull), hh, row, fg, ub);
+      if (have) {
+        const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + row) * kHeadDim) + 2 * j;
+        const float *yh = F.o + h * kHeadDim + 16 * j;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const uint4 w = vr[q];
+          const uint32_t w4[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const float a = bf16_lo(w4[t]) - yh[8 * q + 2 * t];
+            const float b = bf16_hi(w4[t]) - yh[8 * q + 2 * t + 1];
+            d2 = fmaf(a, a, d2);
+            d2 = fmaf(b, b, d2);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) d2 += __shfl_xor(d2, o);
+    if (have && j == 0) F.hs[h * kHs + kHsLb] = fg * sqrtf(d2);
+  }
+  __syncthreads();
+
+  // (4) Every other candidate whose bound exceeds its head's best value: listed, then evaluated
+  //     one per lane (a whole value row each).
+  auto eval_list = [&](int n) {
+    __syncthreads();  // the list is in LDS
+    for (int i = lane; i < n; i += 64) {
+      int h, row;
+      float fg, ub;
+      decode(F.list[i], h, row, fg, ub);
+      asm volatile("" ::: "memory");  // keep yhat in LDS rather than 128 registers
+      const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + row) * kHeadDim);
+      const float *yh = F.o + h * kHeadDim;
+      uint4 vv[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) vv[k] = vr[k];
+      float d2 = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const uint32_t w4[4] = {vv[k].x, vv[k].y, vv[k].z, vv[k].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const float a = bf16_lo(w4[t]) - yh[8 * k + 2 * t];
+          const float b = bf16_hi(w4[t]) - yh[8 * k + 2 * t + 1];
+          d2 = fmaf(a, a, d2);
+          d2 = fmaf(b, b, d2);
+        }
+      }
+      atomicMax(reinterpret_cast<unsigned *>(F.hs + h * kHs + kHsLb), __float_as_uint(fg * sqrtf(d2)));
+    }
+    __syncthreads();
+  };
+  int n = 0;
+  for (int e0 = 0; e0 < E; e0 += 64) {
+    const int e = e0 + lane;
+    int h = 0, row;
+    float fg, ub;
+    bool live = false;
+    if (e < E && decode(e, h, row, fg, ub))
+      live = ub > F.hs[h * kHs + kHsLb] && (unsigned)e != (unsigned)(F.best[h] & 0xffffffffull);
+    const uint64_t m = __ballot(live);
+    if (live) {
+      const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      F.list[n + rank] = e;
+    }
+    n += (int)__popcll(m);
+    if (n > kListCap - 64) {
+      eval_list(n);
+      n = 0;
+    }
+  }
+  if (n > 0) eval_list(n);
+
+  // (5) A chunk whose non-candidate bound f (A + B |yhat|) / l still exceeds the best value is
+  //     rescanned row by row.
+  const float scale2 = L.scale * kLog2e;
+  const int nx = nsp * L.nchunk * GB;
+  bool qloaded = false;
+  for (int x0 = 0; x0 < nx; x0 += 64) {
+    const int x = x0 + lane;  // (s nchunk + k) GB + h
+    bool need = false;
+    if (x < nx) {
+      const int h = x % GB, sk = x / GB, s = sk / L.nchunk, k = sk % L.nchunk;
+      if (k * kChunkRows < min(cnt - s * R, R)) {
+        const float *blk = C.base + s * C.sstride + k * C.kstride + h * C.hstride;
+        const float *hs = F.hs + h * kHs;
+        const float ub = scale_of(blk[kChM], hs[kHsM]) * (blk[kChA] + blk[kChB] * hs[kHsYn]) / hs[kHsL];
+        need = ub > hs[kHsLb];
+      }
+    }
+    uint64_t m = __ballot(need);
+    if (m && !qloaded) {  // q of every head into the Cv slots (no longer needed)
+      for (int e = lane; e < GB * kHeadDim / 2; e += 64) {
+        const int h = e / (kHeadDim / 2), d2 = e % (kHeadDim / 2);
+        const uint32_t qw = reinterpret_cast<const uint32_t *>(L.q + (uh0 + h) * kHeadDim)[d2];
+        F.o[(GB + h) * kHeadDim + 2 * d2] = bf16_lo(qw);
+        F.o[(GB + h) * kHeadDim + 2 * d2 + 1] = bf16_hi(qw);
+      }
+      __syncthreads();
+      qloaded = true;
+    }
+    while (m) {
+      const int xx = x0 + (int)__builtin_ctzll(m);
+      m &= m - 1;
+      const int h = xx % GB, sk = xx / GB, s = sk / L.nchunk, k = sk % L.nchunk;
+      const int ra = s * R + k * kChunkRows;
+      const int rz = min(min(cnt, (s + 1) * R), ra + kChunkRows);
+      const float *hs = F.hs + h * kHs;
+      const float M = hs[kHsM];
+      const float *qh = F.o + (GB + h) * kHeadDim;
+      const float *yh = F.o + h * kHeadDim;
+      const float *blk = C.base + s * C.sstride + k * C.kstride + h * C.hstride;
+      const float fk = scale_of(blk[kChM], M) / hs[kHsL];
+      const float bterm = blk[kChB] * hs[kHsYn];
+      // only the rows of a candidate lane whose own bound still exceeds the best value: lane i
+      // kept row group i % 4 of the chunk's tiles of parity i / 4 (64 rows)
+      const int i = lane >> 3;  // lane group i decides for candidate lane i
+      const float ai = __uint_as_float(
+          ((__float_as_uint(blk[kChAL + (i & 3) / 2 + 2 * (i >> 2)]) >> (16 * (i & 1))) & 0xffffu) << 16);
+      const uint64_t lanes = __ballot((lane & 7) == 0 && fk * (ai + bterm) > hs[kHsLb]);
+      float best = 0.0f;
+      for (uint64_t lm = lanes; lm; lm &= lm - 1) {
+        const int li = (int)__builtin_ctzll(lm) >> 3;
+        if (lane == 0) atomicAdd(L.diag + (int64_t)u * L.nhb + h0 / kHeadBlock, 1u);
+        const int j = ra + 32 * (lane >> 2) + 16 * (li >> 2) + 4 * (li & 3) + (lane & 3);
+        if (j >= rz) continue;
+        const uint4 *kr = reinterpret_cast<const uint4 *>(L.Kc + (cbase + j) * kHeadDim);
+        const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + j) * kHeadDim);
+        const float pj = L.pic[cbase + j];
+        float dot = 0.0f, d2 = 0.0f;
+        for (int half = 0; half < 2; ++half) {  // half a row per step keeps the registers down
+          asm volatile("" ::: "memory");       // q and yhat stay in LDS
+          uint4 kq[8], vq[8];
+#pragma unroll
+          for (int k2 = 0; k2 < 8; ++k2) {
+            kq[k2] = kr[8 * half + k2];
+            vq[k2] = vr[8 * half + k2];
+          }
+#pragma unroll
+          for (int k2 = 0; k2 < 8; ++k2) {
+            const uint32_t kw[4] = {kq[k2].x, kq[k2].y, kq[k2].z, kq[k2].w};
+            const uint32_t vw[4] = {vq[k2].x, vq[k2].y, vq[k2].z, vq[k2].w};
+            const int d0 = 64 * half + 8 * k2;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              dot = fmaf(qh[d0 + 2 * t], bf16_lo(kw[t]), dot);
+              dot = fmaf(qh[d0 + 2 * t + 1], bf16_hi(kw[t]), dot);
+              const float a = bf16_lo(vw[t]) - yh[d0 + 2 * t];
+              const float b = bf16_hi(vw[t]) - yh[d0 + 2 * t + 1];
+              d2 = fmaf(a, a, d2);
+              d2 = fmaf(b, b, d2);
+            }
+          }
+        }
+        const float w = fast_exp2(dot * scale2 - fast_log2(pj) - M);
+        best = fmaxf(best, sqrtf(1.0f - pj) * w * sqrtf(d2));
+      }
+      best = wave_max(best) / hs[kHsL];
+      if (lane == 0) F.hs[h * kHs + kHsLb] = fmaxf(F.hs[h * kHs + kHsLb], best);
+      __syncthreads();
+    }
+  }
+
+  // (6) b and the radius of eq. (4).
+  if (lane < GB) {
+    const float *hs = F.hs + lane * kHs;
+    const float Ld = logf(1.0f / L.delta);
+    const float b = hs[kHsLb];
+    if (L.brange) L.brange[uh0 + lane] = b;
+    if (L.radius) L.radius[uh0 + lane] = (sqrtf(2.0f * hs[kHsV] * Ld) + b * Ld) / (hs[kHsYn] + L.eps0);
+  }
+}
+
+// Outputs of a unit with no retained rows.
+template <int GB>
+__device__ void finalize_empty(const AttendLaunch &L, int u, int h0) {
+  const int lane = threadIdx.x & 63;
+  const int64_t uh0 = (int64_t)u * L.G + h0;
+  for (int e = lane; e < GB * kHeadDim; e += 64) L.y[uh0 * kHeadDim + e] = 0.0f;
+  if (lane < GB) {
+    L.vhat[uh0 + lane] = 0.0f;
+    L.lse[uh0 + lane] = -INFINITY;
+    if (L.brange) L.brange[uh0 + lane] = 0.0f;
+    if (L.radius) L.radius[uh0 + lane] = 0.0f;
+  }
+  if (lane == 0) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+}
+
+// One wave per (unit, split, head block).  Lane (g, c): MFMA column c is head slot c (weights for
+// c < GB, variance weights for GB <= c < 2 GB, idle above); g selects the row group.
+template <int GB>
+__global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int h0) {
+  extern __shared__ float s_chunk[];  // [nchunk][GB][kChunkFloats]
   const int bid = blockIdx.x;
   const int sp = bid % L.nsplit;
   const int u = bid / L.nsplit;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x;
   const int g = lane >> 4, c = lane & 15;
-  if (bid == 0 && tid == 0 && h0 == 0) L.diag[0] = 0u;
-
   const int64_t cbase = L.cap_off[u];
   const int64_t cap = L.cap_off[u + 1] - cbase;
   const int cnt = (int)min(min((int64_t)L.count[u], cap), (int64_t)L.nsplit * L.split_rows);
   const int row0 = sp * L.split_rows;
-  if (row0 >= cnt) return;  // empty split: the finalize pass skips it
-  const int row1 = min(cnt, row0 + L.split_rows);
+  if (row0 >= cnt) {  // empty split: the finalize skips it; an empty unit gets empty outputs
+    if (L.nsplit == 1) finalize_empty<GB>(L, u, h0);
+    return;
+  }
+  const int nrow = min(cnt - row0, L.split_rows);
 
   const bool isW = c < GB;
   const bool isC = (c >= GB) && (c < 2 * GB);
@@ -238,349 +619,214 @@ __global__ __launch_bounds__(kAttendThreads, 2) void attend_split_kernel(AttendL
   }
   S.dk = S.dg = 0.0f;
 
-  const uint4 *Kb = reinterpret_cast<const uint4 *>(L.Kc + cbase * kHeadDim);
-  const uint4 *Vb = reinterpret_cast<const uint4 *>(L.Vc + cbase * kHeadDim);
-  const float *Pb = L.pic + cbase;
+  // The split's rows only: anything past them reads as zero.
+  const int64_t r0 = cbase + row0;
+  const __amdgpu_buffer_rsrc_t rK = make_rsrc(L.Kc + r0 * kHeadDim, (uint32_t)nrow * 256u);
+  const __amdgpu_buffer_rsrc_t rV = make_rsrc(L.Vc + r0 * kHeadDim, (uint32_t)nrow * 256u);
+  const __amdgpu_buffer_rsrc_t rP = make_rsrc(L.pic + r0, (uint32_t)nrow * 4u);
   const float scale2 = L.scale * kLog2e;
-  const int ntile = (row1 - row0 + 15) / 16;
-  const int rlast = row1 - 1;
+  const int ntile = (nrow + 15) / 16;
+  const int nv0 = active ? nrow - 4 * g : -1;  // valid rows of this lane's row group in tile 0
+  const int rb0 = row0 + 4 * g;
 
-  // Two tiles in registers: the next one loads while the current one is computed.  The
-  // prefetch is unconditional (clamped to the last tile) so the compiler can wait for exactly
-  // the current tile's loads.
-  Tile TA, TB;
-  const int tlast = ntile - 1;
-  const int gmask = active ? 0 : (1 << 30);  // inactive columns see no valid rows
-  int tt = wave;
-  if (tt < ntile) load_tile(TA, Kb, Vb, Pb, row0 + 16 * tt, rlast, g, c);
-  while (tt < ntile) {
-    load_tile(TB, Kb, Vb, Pb, row0 + 16 * min(tt + 4, tlast), rlast, g, c);
-    S.rowbase = row0 + 16 * tt + 4 * g;
-    split_tile(S, TA, qop, row1 - S.rowbase - gmask, g, isC, scale2);
-    tt += 4;
-    if (tt >= ntile) break;
-    load_tile(TA, Kb, Vb, Pb, row0 + 16 * min(tt + 4, tlast), rlast, g, c);
-    S.rowbase = row0 + 16 * tt + 4 * g;
-    split_tile(S, TB, qop, row1 - S.rowbase - gmask, g, isC, scale2);
-    tt += 4;
+  // Three tiles in registers: two load while the third is computed.  The loop body is straight
+  // line (whole triples), so the compiler waits for exactly the tile it is about to use.
+  Tile T0, T1, T2;
+  load_tile(T0, rK, rV, rP, 0, g, c);
+  load_tile(T1, rK, rV, rP, 1, g, c);
+  constexpr int kChunkTiles = kChunkRows / 16;
+  // tile tt of the split, then the flush of its chunk if tt ends one
+  auto step = [&](const Tile &T, int tt) {
+    split_tile(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, isC == ((tt & 1) != 0), scale2);
+    if ((tt + 1) % kChunkTiles == 0)
+      flush_chunk<GB>(S, s_chunk, tt / kChunkTiles, g, c, row0 + (tt / kChunkTiles) * kChunkRows);
+  };
+  int t = 0;
+  for (; t + 3 <= ntile; t += 3) {
+    load_tile(T2, rK, rV, rP, t + 2, g, c);
+    step(T0, t);
+    load_tile(T0, rK, rV, rP, t + 3, g, c);
+    step(T1, t + 1);
+    load_tile(T1, rK, rV, rP, t + 4, g, c);
+    step(T2, t + 2);
   }
+  if (t < ntile) step(T0, t);
+  if (t + 1 < ntile) step(T1, t + 1);
+  // every chunk is flushed once: full ones where they end, a partial last one here
+  const int nck = (ntile + kChunkTiles - 1) / kChunkTiles;
+  if (ntile % kChunkTiles != 0)
+    flush_chunk<GB>(S, s_chunk, nck - 1, g, c, row0 + (nck - 1) * kChunkRows);
 
-  // ---- wave results to LDS -------------------------------------------------------------------
+  // ---- epilogue ------------------------------------------------------------------------------
   float s0 = S.s0, s1 = S.s1;
   s0 += __shfl_xor(s0, 16);
   s0 += __shfl_xor(s0, 32);
   s1 += __shfl_xor(s1, 16);
   s1 += __shfl_xor(s1, 32);
-  if (g == 0) {
-    s_m[wave][c] = S.mrun;
-    s_s0[wave][c] = s0;
-    s_s1[wave][c] = s1;
-  }
+  if (L.nsplit == 1) {
+    // The unit is this one split: its sums go to LDS beside the chunk blocks and the wave
+    // finalizes its heads itself (no record, no second launch).
+    FinLds<GB> F(s_chunk + L.nchunk * GB * kChunkFloats);
 #pragma unroll
-  for (int db = 0; db < 8; ++db) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) s_acc[wave][4 * g + i][8 * c + db] = S.acc[db][i];
-  }
-  if (isW) {
-    const int e = wave * 16 + g * 4;  // 64 entries per head: (wave, g, rank)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      s_ck[c][e + q] = S.ck[q];
-      s_cg[c][e + q] = S.cg[q];
-      s_cr[c][e + q] = S.cr[q];
-    }
-    s_dk[c][wave * 4 + g] = S.dk;
-    s_dg[c][wave * 4 + g] = S.dg;
-  }
-  __syncthreads();
-
-  // ---- merge the four waves and write one record per head ------------------------------------
-  float *rec_base = L.part + (((int64_t)u * L.nsplit + sp) * L.G + h0) * kRec;
-  for (int e = tid; e < 2 * GB * kHeadDim; e += kAttendThreads) {
-    const int slot = e / kHeadDim, d = e % kHeadDim;
-    const int hh = slot < GB ? slot : slot - GB;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][hh]);
-    float sum = 0.0f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      float f = scale_of(s_m[w][hh], M);
-      if (slot >= GB) f *= f;
-      sum += f * s_acc[w][slot][d];
-    }
-    rec_base[(int64_t)hh * kRec + (slot < GB ? kRecO : kRecCv) + d] = sum;
-  }
-  // candidates: wave w merges heads w and w + 4 (64 entries -> the kCand largest by rank)
-  for (int hh = wave; hh < GB; hh += 4) {
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][hh]);
-    // keys are squares: scale by f^2, compare, and take square roots only for what is stored
-    float f = scale_of(s_m[lane >> 4][hh], M);
-    f *= f;
-    const int row = s_cr[hh][lane];
-    const float k = row >= 0 ? f * s_ck[hh][lane] : 0.0f;
-    const float gv = row >= 0 ? f * s_cg[hh][lane] : 0.0f;
-    s_key[wave][lane] = k;  // written and read by this wave only
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the keys are in LDS
-    int rank = 0;
-    const float4 *kk = reinterpret_cast<const float4 *>(s_key[wave]);
-#pragma unroll 4
-    for (int e4 = 0; e4 < 16; ++e4) {
-      const float4 q = kk[e4];
-      const float qe[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int e = 4 * e4 + t;
-        rank += (qe[t] > k || (qe[t] == k && e < lane)) ? 1 : 0;
+    for (int i = 0; i < 4; ++i) {
+      const int slot = 4 * g + i;
+      if (slot < 2 * GB) {
+        float4 *dst = reinterpret_cast<float4 *>(F.o + slot * kHeadDim + 8 * c);
+        dst[0] = make_float4(S.acc[0][i], S.acc[1][i], S.acc[2][i], S.acc[3][i]);
+        dst[1] = make_float4(S.acc[4][i], S.acc[5][i], S.acc[6][i], S.acc[7][i]);
       }
     }
-    const bool chosen = row >= 0 && k > 0.0f && rank < kCand;
-    float dA = chosen ? 0.0f : k, dB = chosen ? 0.0f : gv;
-    if (lane < 16) {
-      float fw = scale_of(s_m[lane >> 2][hh], M);
-      fw *= fw;
-      dA = fmaxf(dA, fw * s_dk[hh][lane]);
-      dB = fmaxf(dB, fw * s_dg[hh][lane]);
+    if (g == 0 && isW) {
+      F.hs[c * kHs + kHsM] = S.mrun;
+      F.hs[c * kHs + kHsL] = s0;
+    } else if (g == 0 && isC) {
+      F.hs[(c - GB) * kHs + kHsC0] = s0;
+      F.hs[(c - GB) * kHs + kHsC2] = s1;
     }
-    dA = sqrtf(wave_max(dA));
-    dB = sqrtf(wave_max(dB));
-    const float vmax = sqrtf(wave_max(chosen && gv > 0.0f ? k / gv : 0.0f));
-    // chosen ranks are distinct and < kCand; unfilled candidate slots get row -1
-    const int nchosen = __popcll(__ballot(chosen));
-    float *rec = rec_base + (int64_t)hh * kRec;
-    if (chosen) {
-      rec[kRecCandG + rank] = sqrtf(gv);
-      rec[kRecCandI + rank] = __int_as_float(row);
-    }
-    if (lane == 0) rec[kRecVmax] = vmax;
-    if (lane >= nchosen && lane < kCand) {
-      rec[kRecCandG + lane] = 0.0f;
-      rec[kRecCandI + lane] = __int_as_float(-1);
-    }
-    if (lane == 0) {
-      float lsum = 0.0f, c0 = 0.0f, c2 = 0.0f;
+    if (lane == 0) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+    __syncthreads();
+    const CandSrc C{s_chunk, 0, GB * kChunkFloats, kChunkFloats};
+    finalize_block<GB>(L, u, h0, cnt, cbase, 1, C, F);
+    return;
+  }
+  // Several splits: this one's record (sums from registers, chunk blocks from LDS).
+  float *rec_base = L.part + (((int64_t)u * L.nsplit + sp) * L.G + h0) * L.rec;
+  // o (slots < GB) and Cv (slots GB .. 2GB-1): lane (g, c) holds slots 4g + i, dims 8c .. 8c + 7
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float fw = scale_of(s_m[w][hh], M);
-        lsum += fw * s_s0[w][hh];
-        c0 += fw * fw * s_s0[w][GB + hh];
-        c2 += fw * fw * s_s1[w][GB + hh];
-      }
-      rec[kRecM] = M;
-      rec[kRecL] = lsum;
-      rec[kRecC0] = c0;
-      rec[kRecC2] = c2;
-      rec[kRecA] = dA;
-      rec[kRecB] = dB;
+  for (int i = 0; i < 4; ++i) {
+    const int slot = 4 * g + i;
+    if (slot < 2 * GB) {
+      const int hh = slot < GB ? slot : slot - GB;
+      float4 *dst = reinterpret_cast<float4 *>(rec_base + (int64_t)hh * L.rec +
+                                               (slot < GB ? kRecO : kRecCv) + 8 * c);
+      dst[0] = make_float4(S.acc[0][i], S.acc[1][i], S.acc[2][i], S.acc[3][i]);
+      dst[1] = make_float4(S.acc[4][i], S.acc[5][i], S.acc[6][i], S.acc[7][i]);
     }
+  }
+  if (g == 0 && isW) {
+    float *rec = rec_base + (int64_t)c * L.rec;
+    rec[kRecM] = S.mrun;
+    rec[kRecL] = s0;
+  } else if (g == 0 && isC) {
+    float *rec = rec_base + (int64_t)(c - GB) * L.rec;
+    rec[kRecC0] = s0;
+    rec[kRecC2] = s1;
+  }
+  __syncthreads();  // the chunk blocks are in LDS
+  const int nblk = nck * GB * kChunkFloats;
+  for (int e = lane; e < nblk; e += 64) {
+    const int k = e / (GB * kChunkFloats), r = e % (GB * kChunkFloats);
+    const int hh = r / kChunkFloats, j = r % kChunkFloats;
+    rec_base[(int64_t)hh * L.rec + kRecChunks + k * kChunkFloats + j] = s_chunk[e];
   }
 }
 
-// ---------------------------------------------------------------------------------------------
-// attend_finalize: one wave per (unit, query head)
-// ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void attend_finalize_kernel(AttendLaunch L) {
-  __shared__ float s_y[kHeadDim];
-  __shared__ float s_q[kHeadDim];
-  const int64_t bid = blockIdx.x;
-  const int u = (int)(bid / L.G), h = (int)(bid % L.G);
+// attend_finalize: one wave per (unit, head block) when units are cut into several splits; the
+// split records are combined into LDS, then finalized like a fused split.
+template <int GB>
+__global__ __launch_bounds__(64) void attend_finalize_kernel(AttendLaunch L, int h0) {
+  extern __shared__ float s_fin[];
+  const int u = blockIdx.x;
   const int lane = threadIdx.x;
-  const int64_t uh = bid;
   const int64_t cbase = L.cap_off[u];
   const int64_t cap = L.cap_off[u + 1] - cbase;
   const int cnt = (int)min(min((int64_t)L.count[u], cap), (int64_t)L.nsplit * L.split_rows);
-  float2 *yout = reinterpret_cast<float2 *>(L.y + uh * kHeadDim);
   if (cnt == 0) {
-    yout[lane] = make_float2(0.0f, 0.0f);
-    if (lane == 0) {
-      L.vhat[uh] = 0.0f;
-      L.lse[uh] = -INFINITY;
-      if (L.brange) L.brange[uh] = 0.0f;
-      if (L.radius) L.radius[uh] = 0.0f;
-    }
+    finalize_empty<GB>(L, u, h0);
     return;
   }
+  if (lane == 0) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
   const int nsp = (cnt + L.split_rows - 1) / L.split_rows;
-  const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h) * kRec;
-  const int64_t rstride = (int64_t)L.G * kRec;
+  const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h0) * L.rec;  // (s, h) at s G rec + h rec
+  const int64_t sstride = (int64_t)L.G * L.rec;
+  FinLds<GB> F(s_fin);
 
-  float M = -INFINITY;
-  for (int s = lane; s < nsp; s += 64) M = fmaxf(M, rec0[s * rstride + kRecM]);
-  M = wave_max(M);
-  float l = 0.0f, C0 = 0.0f, C2 = 0.0f;
-  for (int s = lane; s < nsp; s += 64) {
-    const float *r = rec0 + s * rstride;
-    const float f = scale_of(r[kRecM], M);
-    l += f * r[kRecL];
-    C0 += f * f * r[kRecC0];
-    C2 += f * f * r[kRecC2];
+  // combined scalars: lane (h, s) pairs; M first, then the scaled sums
+  for (int h = 0; h < GB; ++h) {
+    float M = -INFINITY;
+    for (int s = lane; s < nsp; s += 64) M = fmaxf(M, rec0[s * sstride + h * L.rec + kRecM]);
+    M = wave_max(M);
+    float l = 0.0f, c0 = 0.0f, c2 = 0.0f;
+    for (int s = lane; s < nsp; s += 64) {
+      const float *r = rec0 + s * sstride + h * L.rec;
+      const float f = scale_of(r[kRecM], M);
+      l += f * r[kRecL];
+      c0 += f * f * r[kRecC0];
+      c2 += f * f * r[kRecC2];
+    }
+    l = wave_sum(l);
+    c0 = wave_sum(c0);
+    c2 = wave_sum(c2);
+    if (lane == 0) {
+      F.hs[h * kHs + kHsM] = M;
+      F.hs[h * kHs + kHsL] = l;
+      F.hs[h * kHs + kHsC0] = c0;
+      F.hs[h * kHs + kHsC2] = c2;
+    }
   }
-  l = wave_sum(l);
-  C0 = wave_sum(C0);
-  C2 = wave_sum(C2);
-
-  float2 o = make_float2(0.0f, 0.0f), cv = make_float2(0.0f, 0.0f);
-  for (int s = 0; s < nsp; ++s) {
-    const float *r = rec0 + s * rstride;
-    const float f = scale_of(r[kRecM], M);
-    const float2 a = reinterpret_cast<const float2 *>(r + kRecO)[lane];
-    const float2 b = reinterpret_cast<const float2 *>(r + kRecCv)[lane];
-    o.x += f * a.x;
-    o.y += f * a.y;
-    cv.x += f * f * b.x;
-    cv.y += f * f * b.y;
-  }
-  const float y0 = o.x / l, y1 = o.y / l;
-  s_y[2 * lane] = y0;
-  s_y[2 * lane + 1] = y1;
-  {
-    const uint32_t qw = reinterpret_cast<const uint32_t *>(L.q + uh * kHeadDim)[lane];
-    s_q[2 * lane] = bf16_lo(qw);
-    s_q[2 * lane + 1] = bf16_hi(qw);
-  }
-  const float ynorm2 = wave_sum(y0 * y0 + y1 * y1);
-  const float ycv = wave_sum(y0 * cv.x + y1 * cv.y);
-  const float V = fmaxf(C2 - 2.0f * ycv + ynorm2 * C0, 0.0f) / (l * l);
-  const float ynorm = sqrtf(ynorm2);
   __syncthreads();
-
-  // Range term, exact at the candidate rows.  A candidate's value f g |v - yhat| / l is at most
-  // f g (Vmax + |yhat|) / l; the most promising candidate is evaluated first (whole wave), then
-  // only the candidates whose bound still exceeds the best value so far (one per lane).
-  const uint16_t *Vrows = L.Vc + cbase * kHeadDim;
-  const int ncand = nsp * kCand;
-  auto cand_bound = [&](int e, int &row, float &fg) -> float {
-    const float *r = rec0 + (e / kCand) * rstride;
-    row = __float_as_int(r[kRecCandI + (e % kCand)]);
-    fg = scale_of(r[kRecM], M) * r[kRecCandG + (e % kCand)] / l;
-    return row >= 0 ? fg * (r[kRecVmax] + ynorm) : 0.0f;
-  };
-  // the candidate with the largest bound, by the whole wave
-  float best_ub = 0.0f;
-  int best_e = -1;
-  for (int e = lane; e < ncand; e += 64) {
-    int row;
-    float fg;
-    const float ub = cand_bound(e, row, fg);
-    if (ub > best_ub) {
-      best_ub = ub;
-      best_e = e;
+  // combined o and Cv: slot-major, two dims per lane
+  for (int slot = 0; slot < 2 * GB; ++slot) {
+    const int h = slot < GB ? slot : slot - GB;
+    const int off = slot < GB ? kRecO : kRecCv;
+    const float M = F.hs[h * kHs + kHsM];
+    float2 acc = make_float2(0.0f, 0.0f);
+    for (int s = 0; s < nsp; ++s) {
+      const float *r = rec0 + s * sstride + h * L.rec;
+      float f = scale_of(r[kRecM], M);
+      if (slot >= GB) f *= f;
+      const float2 a = reinterpret_cast<const float2 *>(r + off)[lane];
+      acc.x += f * a.x;
+      acc.y += f * a.y;
     }
+    reinterpret_cast<float2 *>(F.o + slot * kHeadDim)[lane] = acc;
   }
-  {
-    const float m = wave_max(best_ub);
-    const uint64_t who = __ballot(best_ub == m && best_e >= 0);
-    best_e = who ? __shfl(best_e, (int)__ffsll((unsigned long long)who) - 1) : -1;
-  }
-  float lb = 0.0f;
-  if (best_e >= 0) {
-    int row;
-    float fg;
-    cand_bound(best_e, row, fg);
-    const uint32_t w = reinterpret_cast<const uint32_t *>(Vrows + (int64_t)row * kHeadDim)[lane];
-    const float d0 = bf16_lo(w) - y0, d1 = bf16_hi(w) - y1;
-    lb = fg * sqrtf(wave_sum(d0 * d0 + d1 * d1));
-  }
-  for (int e = lane; e < ncand; e += 64) {
-    int row;
-    float fg;
-    const float ub = cand_bound(e, row, fg);
-    if (!(ub > lb) || e == best_e) continue;
-    // keep yhat in LDS (re-read per candidate) instead of 128 registers
-    asm volatile("" ::: "memory");
-    const uint4 *vr = reinterpret_cast<const uint4 *>(Vrows + (int64_t)row * kHeadDim);
-    uint4 vv[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) vv[k] = vr[k];
-    float d2 = 0.0f;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const uint32_t w4[4] = {vv[k].x, vv[k].y, vv[k].z, vv[k].w};
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float a = bf16_lo(w4[t]) - s_y[8 * k + 2 * t];
-        const float b = bf16_hi(w4[t]) - s_y[8 * k + 2 * t + 1];
-        d2 = fmaf(a, a, d2);
-        d2 = fmaf(b, b, d2);
-      }
-    }
-    lb = fmaxf(lb, fg * sqrtf(d2));
-  }
-  lb = wave_max(lb);
-  // ... and a rescan of any split whose bound max(g|v|) + max(g)|yhat| could exceed it.
-  const float scale2 = L.scale * kLog2e;
-  for (int s = 0; s < nsp; ++s) {
-    const float *r = rec0 + s * rstride;
-    const float f = scale_of(r[kRecM], M);
-    const float ub = f * (r[kRecA] + r[kRecB] * ynorm) / l;
-    if (!(ub > lb)) continue;
-    if (lane == 0) atomicAdd(L.diag, 1u);
-    const int ra = s * L.split_rows, rz = min(cnt, ra + L.split_rows);
-    const float ms = r[kRecM];
-    float best = 0.0f;
-    for (int j = ra + lane; j < rz; j += 64) {
-      const uint4 *kr = reinterpret_cast<const uint4 *>(L.Kc + (cbase + j) * kHeadDim);
-      const uint4 *vr = reinterpret_cast<const uint4 *>(Vrows + (int64_t)j * kHeadDim);
-      const float pj = L.pic[cbase + j];
-      float dot = 0.0f, d2 = 0.0f;
-      for (int half = 0; half < 2; ++half) {  // half a row per step keeps the registers down
-        asm volatile("" ::: "memory");  // q and yhat stay in LDS
-        uint4 kq[8], vq[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          kq[k] = kr[8 * half + k];
-          vq[k] = vr[8 * half + k];
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const uint32_t kw[4] = {kq[k].x, kq[k].y, kq[k].z, kq[k].w};
-          const uint32_t vw[4] = {vq[k].x, vq[k].y, vq[k].z, vq[k].w};
-          const int d0 = 64 * half + 8 * k;
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            dot = fmaf(s_q[d0 + 2 * t], bf16_lo(kw[t]), dot);
-            dot = fmaf(s_q[d0 + 2 * t + 1], bf16_hi(kw[t]), dot);
-            const float a = bf16_lo(vw[t]) - s_y[d0 + 2 * t];
-            const float b = bf16_hi(vw[t]) - s_y[d0 + 2 * t + 1];
-            d2 = fmaf(a, a, d2);
-            d2 = fmaf(b, b, d2);
-          }
-        }
-      }
-      const float w = fast_exp2(dot * scale2 - fast_log2(pj) - ms);
-      best = fmaxf(best, sqrtf(1.0f - pj) * w * sqrtf(d2));
-    }
-    lb = fmaxf(lb, wave_max(f * best / l));
-  }
-  const float Ld = logf(1.0f / L.delta);
-  yout[lane] = make_float2(y0, y1);
-  if (lane == 0) {
-    L.vhat[uh] = V;
-    L.lse[uh] = M * kLn2 + logf(l);
-    if (L.brange) L.brange[uh] = lb;
-    if (L.radius) L.radius[uh] = (sqrtf(2.0f * V * Ld) + lb * Ld) / (ynorm + L.eps0);
-  }
+  __syncthreads();
+  const CandSrc C{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
+  finalize_block<GB>(L, u, h0, cnt, cbase, nsp, C, F);
 }
 
-size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G) {
-  return 256 + (size_t)U * (size_t)nsplit * (size_t)G * kRec * sizeof(float);
+size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows) {
+  const size_t nhb = (size_t)((G + kHeadBlock - 1) / kHeadBlock);
+  const size_t diag = ((size_t)U * nhb * sizeof(uint32_t) + 255) / 256 * 256;
+  if (nsplit <= 1) return diag;  // fused: no split records
+  return diag + (size_t)U * (size_t)nsplit * (size_t)G * (size_t)attend_record_floats(split_rows) *
+                    sizeof(float);
+}
+
+size_t attend_split_lds(const AttendLaunch &L, int gb) {
+  size_t b = (size_t)L.nchunk * gb * kChunkFloats * sizeof(float);
+  if (L.nsplit == 1) {
+    size_t f = 0;
+    switch (gb) {
+      case 1: f = FinLds<1>::bytes(); break;
+      case 2: f = FinLds<2>::bytes(); break;
+      case 3: f = FinLds<3>::bytes(); break;
+      case 4: f = FinLds<4>::bytes(); break;
+      case 5: f = FinLds<5>::bytes(); break;
+      case 6: f = FinLds<6>::bytes(); break;
+      case 7: f = FinLds<7>::bytes(); break;
+      default: f = FinLds<8>::bytes(); break;
+    }
+    b += f;
+  }
+  return b;
 }
 
 hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)L.U * L.nsplit)), block(kAttendThreads);
   for (int h0 = 0; h0 < L.G; h0 += kHeadBlock) {
     const int gb = min(kHeadBlock, L.G - h0);
+    const size_t lds = attend_split_lds(L, gb);
     switch (gb) {
-      case 1: hipLaunchKernelGGL(attend_split_kernel<1>, grid, block, 0, s, L, h0); break;
-      case 2: hipLaunchKernelGGL(attend_split_kernel<2>, grid, block, 0, s, L, h0); break;
-      case 3: hipLaunchKernelGGL(attend_split_kernel<3>, grid, block, 0, s, L, h0); break;
-      case 4: hipLaunchKernelGGL(attend_split_kernel<4>, grid, block, 0, s, L, h0); break;
-      case 5: hipLaunchKernelGGL(attend_split_kernel<5>, grid, block, 0, s, L, h0); break;
-      case 6: hipLaunchKernelGGL(attend_split_kernel<6>, grid, block, 0, s, L, h0); break;
-      case 7: hipLaunchKernelGGL(attend_split_kernel<7>, grid, block, 0, s, L, h0); break;
-      default: hipLaunchKernelGGL(attend_split_kernel<8>, grid, block, 0, s, L, h0); break;
+      case 1: hipLaunchKernelGGL(attend_split_kernel<1>, grid, block, lds, s, L, h0); break;
+      case 2: hipLaunchKernelGGL(attend_split_kernel<2>, grid, block, lds, s, L, h0); break;
+      case 3: hipLaunchKernelGGL(attend_split_kernel<3>, grid, block, lds, s, L, h0); break;
+      case 4: hipLaunchKernelGGL(attend_split_kernel<4>, grid, block, lds, s, L, h0); break;
+      case 5: hipLaunchKernelGGL(attend_split_kernel<5>, grid, block, lds, s, L, h0); break;
+      case 6: hipLaunchKernelGGL(attend_split_kernel<6>, grid, block, lds, s, L, h0); break;
+      case 7: hipLaunchKernelGGL(attend_split_kernel<7>, grid, block, lds, s, L, h0); break;
+      default: hipLaunchKernelGGL(attend_split_kernel<8>, grid, block, lds, s, L, h0); break;
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -589,8 +835,23 @@ hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s) {
 }
 
 hipError_t launch_attend_finalize(const AttendLaunch &L, hipStream_t s) {
-  hipLaunchKernelGGL(attend_finalize_kernel, dim3((unsigned)((int64_t)L.U * L.G)), dim3(64), 0, s, L);
-  return hipGetLastError();
+  const dim3 grid((unsigned)L.U), block(64);
+  for (int h0 = 0; h0 < L.G; h0 += kHeadBlock) {
+    const int gb = min(kHeadBlock, L.G - h0);
+    switch (gb) {
+      case 1: hipLaunchKernelGGL(attend_finalize_kernel<1>, grid, block, FinLds<1>::bytes(), s, L, h0); break;
+      case 2: hipLaunchKernelGGL(attend_finalize_kernel<2>, grid, block, FinLds<2>::bytes(), s, L, h0); break;
+      case 3: hipLaunchKernelGGL(attend_finalize_kernel<3>, grid, block, FinLds<3>::bytes(), s, L, h0); break;
+      case 4: hipLaunchKernelGGL(attend_finalize_kernel<4>, grid, block, FinLds<4>::bytes(), s, L, h0); break;
+      case 5: hipLaunchKernelGGL(attend_finalize_kernel<5>, grid, block, FinLds<5>::bytes(), s, L, h0); break;
+      case 6: hipLaunchKernelGGL(attend_finalize_kernel<6>, grid, block, FinLds<6>::bytes(), s, L, h0); break;
+      case 7: hipLaunchKernelGGL(attend_finalize_kernel<7>, grid, block, FinLds<7>::bytes(), s, L, h0); break;
+      default: hipLaunchKernelGGL(attend_finalize_kernel<8>, grid, block, FinLds<8>::bytes(), s, L, h0); break;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace ebd

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -81,17 +82,18 @@ hipError_t timed(const char *name, hipStream_t s, F &&launch) {
 // The sampler keeps no state between its two launches except the index list it writes.
 constexpr size_t kEvictWorkspace = 256;
 
-// Rows per split: at most 1024, halved (down to 256) until the grid has >= 2048 work-groups
-// (eight per compute unit), unless the caller fixes it.
+// Rows per split (a multiple of 16).  Unless the caller fixes it: one split per unit when there
+// are enough units for kSplitWaves waves, else units are cut into equal splits until there are;
+// splits stay within [kSplitMinRows, kSplitMaxRows] rows.
 int32_t attend_split_rows(const ebd_attend_params *p) {
   if (p->split_rows > 0) return p->split_rows;
-  int32_t sr = 1024;
-  while (sr > 256) {
-    const int64_t ns = (p->max_rows + sr - 1) / sr;
-    if ((int64_t)p->num_units * (ns > 0 ? ns : 1) >= 2048) break;
-    sr /= 2;
-  }
-  return sr;
+  const int64_t cap = p->max_rows > 0 ? p->max_rows : 1;
+  const int64_t U = p->num_units > 0 ? p->num_units : 1;
+  int64_t ns = (kSplitWaves + U - 1) / U;
+  ns = std::max<int64_t>(ns, (cap + kSplitMaxRows - 1) / kSplitMaxRows);
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, cap / kSplitMinRows));
+  const int64_t sr = ((cap + ns - 1) / ns + 15) / 16 * 16;
+  return (int32_t)sr;
 }
 
 int32_t attend_nsplit(const ebd_attend_params *p, int32_t sr) {
@@ -116,7 +118,8 @@ bool valid_attend_params(const ebd_attend_params *p) {
   if (p->num_units < 0 || p->group < 1 || p->max_rows < 0 || p->max_rows > ((int64_t)1 << 31))
     return false;
   if (p->num_units > 0 && !p->cap_off) return false;
-  if (p->split_rows != 0 && (p->split_rows < 64 || p->split_rows > 65536 || p->split_rows % 64))
+  if (p->split_rows != 0 &&
+      (p->split_rows < 16 || p->split_rows > kSplitRowsLimit || p->split_rows % 16))
     return false;
   if (p->flags != 0u) return false;
   if (p->scale < 0.0f || !std::isfinite(p->scale)) return false;
@@ -152,7 +155,7 @@ size_t ebd_workspace_size(int32_t which, const void *params) {
     const ebd_attend_params *p = static_cast<const ebd_attend_params *>(params);
     if (!valid_attend_params(p)) return 0;
     const int32_t sr = attend_split_rows(p);
-    return attend_workspace_bytes(p->num_units, attend_nsplit(p, sr), p->group);
+    return attend_workspace_bytes(p->num_units, attend_nsplit(p, sr), p->group, sr);
   }
   return 0;
 }
@@ -218,11 +221,11 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
   if (p->num_units == 0) return EBD_OK;
   if (!q || !Kc || !Vc || !pic || !count || !y || !vhat || !lse) return EBD_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(pic, 4) ||
-      !aligned(y, 4))
+      !aligned(y, 16))
     return EBD_ERR_INVALID_ARG;
   const int32_t sr = attend_split_rows(p);
   const int32_t nsplit = attend_nsplit(p, sr);
-  const size_t need = attend_workspace_bytes(p->num_units, nsplit, p->group);
+  const size_t need = attend_workspace_bytes(p->num_units, nsplit, p->group, sr);
   if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
   const ebd_status ds = check_device();
   if (ds != EBD_OK) return ds;
@@ -232,6 +235,8 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
   L.G = p->group;
   L.nsplit = nsplit;
   L.split_rows = sr;
+  L.nchunk = attend_chunks(sr);
+  L.rec = attend_record_floats(sr);
   L.nhb = (p->group + kHeadBlock - 1) / kHeadBlock;
   L.cap_off = p->cap_off;
   L.count = count;
@@ -244,7 +249,7 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
   L.eps0 = p->eps0 > 0.0f ? p->eps0 : 1e-9f;
   char *ws = static_cast<char *>(workspace);
   L.diag = reinterpret_cast<uint32_t *>(ws);
-  L.part = reinterpret_cast<float *>(ws + 256);
+  L.part = reinterpret_cast<float *>(ws + attend_workspace_bytes(p->num_units, 1, p->group, sr));
   L.y = y;
   L.vhat = vhat;
   L.lse = lse;
@@ -254,7 +259,8 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (timed("attend_split", s, [&] { return launch_attend_split(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
-  if (timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
+  if (L.nsplit > 1 &&
+      timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
   return EBD_OK;
 }

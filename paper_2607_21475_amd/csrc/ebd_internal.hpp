@@ -13,21 +13,36 @@ constexpr int kSelectThreads = 256;          // evict_select: four waves per uni
 constexpr int kCopyThreads = 256;            // evict_copy: 16 lanes per 256-byte row
 constexpr int kCopyRows = 128;               // retained rows per evict_copy work-group
 
-constexpr int kAttendThreads = 256;  // four waves per (unit, split, head block)
+constexpr int kAttendThreads = 64;   // one wave per (unit, split, head block)
 constexpr int kHeadBlock = 8;        // query heads handled together (MFMA rows: 8 weight + 8 variance)
-constexpr int kCand = 32;            // range-term candidates kept per (split, head)
-constexpr int kRec = 328;            // floats per (unit, split, head) partial record
+constexpr int kSplitMaxRows = 4096;  // default split length cap (bounds the launch's tail)
+constexpr int kSplitMinRows = 256;   // default split length floor
+constexpr int kSplitWaves = 1536;    // default: cut units until the launch has this many waves
+constexpr int kSplitRowsLimit = 8192;  // largest split a caller may ask for (LDS of one wave)
+constexpr int kChunkRows = 512;      // range-term candidates are kept per chunk of a split
+constexpr int kCand = 32;            // candidates per (chunk, head)
 
-// Partial record layout (floats), logits in base 2:
-//   [0] m  running logit max        [1] l  = sum w        (scale 2^{-m})
+// Partial record per (unit, split, head), floats, logits in base 2:
+//   [0] m  final running max        [1] l  = sum w        (scale 2^{-m})
 //   [2] C0 = sum c                  [3] C2 = sum c |v|^2  (scale 2^{-2m})
-//   [4] A  max over non-candidates of g |v|   [5] B  max over non-candidates of g
-//   [6] Vmax  max |v| over the candidates
-//   [8..39] candidate g             [40..71] candidate row (int bits, -1 = none)
-//   [72..199] o = sum w v           [200..327] Cv = sum c v
+//   [8..135] o = sum w v            [136..263] Cv = sum c v
+//   then one block of kChunkFloats per chunk of kChunkRows rows:
+//     [0] A  max over the chunk's non-candidates of g |v|   [1] B  ... of g
+//     [2] Vmax  max |v| over the candidates   [3] m_k  running max the block is scaled by
+//     [4..35] candidate g (0 = no candidate)  [36..51] candidate rows, two 16-bit offsets from
+//     the chunk's first row per word (candidate j in word j / 2, half j % 2)
+//     [52..55] A of each of the 8 lanes that kept candidates (bf16 rounded up, two per word:
+//     lane i in word i / 2, half i % 2; lane i owns row group i % 4 of the tiles of parity i / 4)
 //   with w = 2^(l2 - m), c = (1 - pi) w^2, g = sqrt(1 - pi) w.
-constexpr int kRecM = 0, kRecL = 1, kRecC0 = 2, kRecC2 = 3, kRecA = 4, kRecB = 5, kRecVmax = 6;
-constexpr int kRecCandG = 8, kRecCandI = 40, kRecO = 72, kRecCv = 200;
+constexpr int kRecM = 0, kRecL = 1, kRecC0 = 2, kRecC2 = 3, kRecO = 8, kRecCv = 136;
+constexpr int kRecChunks = 264;
+constexpr int kChunkFloats = 56;
+constexpr int kChA = 0, kChB = 1, kChVmax = 2, kChM = 3, kChG = 4, kChI = 36, kChAL = 52;
+
+inline int32_t attend_chunks(int32_t split_rows) { return (split_rows + kChunkRows - 1) / kChunkRows; }
+inline int32_t attend_record_floats(int32_t split_rows) {
+  return kRecChunks + kChunkFloats * attend_chunks(split_rows);
+}
 
 struct EvictLaunch {
   int32_t U;
@@ -57,12 +72,13 @@ struct EvictLaunch {
 
 struct AttendLaunch {
   int32_t U, G, nsplit, split_rows, nhb;
+  int32_t nchunk, rec;  // chunks per split, floats per record
   const int64_t *cap_off;
   const int32_t *count;
   const uint16_t *q, *Kc, *Vc;
   const float *pic;
   float scale, delta, eps0;
-  float *part;          // [U * nsplit * G * kRec]
+  float *part;          // [U * nsplit * G * rec]
   uint32_t *diag;       // [0]: number of split rescans taken for the range term
   float *y, *vhat, *lse, *brange, *radius;
 };
@@ -79,7 +95,7 @@ struct AppendLaunch {
   uint32_t *status;
 };
 
-size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G);
+size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows);
 
 hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s);
 hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s);

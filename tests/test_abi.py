@@ -130,7 +130,26 @@ def test_workspace_sizes():
     a.num_units, a.group, a.head_dim, a.max_rows, a.cap_off = 1792, 7, 128, 1856, FAKE
     a.delta = 0.1
     m = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a)
-    assert m == 256 + 1792 * 2 * 7 * 328 * 4  # two splits of 1024 rows, 328-float records
+
+    def rec(split_rows):  # floats per record: sums, o, Cv, one block per 512-row chunk
+        return 264 + 56 * ((split_rows + 511) // 512)
+
+    def counts(U, G):  # rescan counts per (unit, block of 8 query heads), 256-byte padded
+        return (4 * U * ((G + 7) // 8) + 255) // 256 * 256
+
+    # 1792 units fill the chip: one split each, finalized in the split kernel (no records)
+    assert m == counts(1792, 7)
+    a.num_units, a.max_rows = 8, 1024
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(8, 7) + 8 * 4 * 7 * rec(256) * 4
+    a.num_units, a.max_rows = 1024, 13760
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 7) + 1024 * 4 * 7 * rec(3440) * 4
+    a.split_rows = 48
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 7) + 1024 * 287 * 7 * rec(48) * 4
+    a.group = 12  # two head blocks
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 12) + 1024 * 287 * 12 * rec(48) * 4
+    for bad in (40, 8208):  # not a multiple of 16; longer than a wave's candidate store
+        a.split_rows = bad
+        assert lib.ebd_workspace_size(ebd.EBD_WS_ATTEND, ctypes.byref(a)) == 0
     assert lib.ebd_workspace_size(7, ctypes.byref(a)) == 0
 
 

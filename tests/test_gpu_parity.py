@@ -221,6 +221,8 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([2048, 777, 100, 5, 9000, 3000], 8, 0.3, 128),  # ragged tails, G = 8
     ([3000, 1500], 12, 0.2, 0),                # two head blocks (8 + 4)
     ([4096, 300], 9, 0.5, 256),                # 8 + 1
+    ([6144] * 6, 7, 0.5, 512),                 # a candidate chunk ends on the loop's last tiles
+    ([8192] * 3, 4, 0.5, 2048),                # four chunks per split, the last one likewise
 ])
 def test_attend_parity(lengths, G, budget, split):
     _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))
@@ -265,7 +267,7 @@ def test_attend_range_term_rescan_path():
     out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.2, seed=8)
     res = cache.attend_certify(out, q, split_rows=128)
     torch.cuda.synchronize()
-    assert cache.rescans(res["ws"]) > 0
+    assert cache.rescans(res["ws"], U, G) > 0
     _check_attend(out, res, q, G)
 
 
@@ -369,3 +371,138 @@ def test_qwen7b_full_size_sampled_units():
         del out, res
     del inp
     torch.cuda.empty_cache()
+
+
+def _check_unit_end_to_end(u, sl, scores, K, V, pi_all, out, budget, n_sink, n_recent, pi_min,
+                           seed=0, appended=()):
+    """One sampled unit: pi against the oracle's solve, then the oracle's mask, compaction and
+    appended certain rows give the retained set the GPU holds (bit-exact)."""
+    s = _np(scores[sl])
+    pi_ref, _, _ = oracle.inclusion_probs(s, n_sink, n_recent, budget, pi_min)
+    assert np.max(np.abs(pi_all[sl] - pi_ref)) <= 1e-5
+    Kb, Vb = _bits(K[sl]), _bits(V[sl])
+    m = oracle.mask(pi_all[sl], seed, int(u), 0)
+    Kc_r, Vc_r, pic_r, idx_r, c_r = oracle.compact(m, pi_all[sl], Kb, Vb)
+    a = int(_np(out.cap_off[u:u + 1])[0])
+    c = c_r + len(appended)
+    assert int(_np(out.count[u:u + 1])[0]) == c
+    if appended:
+        Kc_r = np.concatenate([Kc_r] + [k[None] for k, _, _ in appended])
+        Vc_r = np.concatenate([Vc_r] + [v[None] for _, v, _ in appended])
+        pic_r = np.concatenate([pic_r, np.ones(len(appended), np.float32)])
+        idx_r = np.concatenate([idx_r, np.array([p for _, _, p in appended], np.int32)])
+    np.testing.assert_array_equal(_np(out.idxc[a:a + c]), idx_r)
+    np.testing.assert_array_equal(_np(out.pic[a:a + c]).view(np.uint32), pic_r.view(np.uint32))
+    np.testing.assert_array_equal(_bits(out.Kc[a:a + c]), Kc_r)
+    np.testing.assert_array_equal(_bits(out.Vc[a:a + c]), Vc_r)
+    return Kc_r, Vc_r, pic_r
+
+
+def _check_unit_attend(u, q, res, Kc_r, Vc_r, pic_r):
+    ref = oracle.attend_certify(_bits(q[u]), Kc_r, Vc_r, pic_r)
+    y = _np(res["y"][u]).astype(np.float64)
+    err = np.linalg.norm(y - ref["y"], axis=1) / np.linalg.norm(ref["y"], axis=1)
+    assert np.all(err <= 2e-3), (u, err)
+    for key in ("vhat", "b", "r"):
+        g = _np(res[key][u]).astype(np.float64)
+        floor = 1e-6 * np.linalg.norm(ref["y"], axis=1) ** (2 if key == "vhat" else 1)
+        assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.maximum(np.abs(ref[key]), floor)), (key, u, g, ref[key])
+    lse = _np(res["lse"][u]).astype(np.float64)
+    assert np.all(np.abs(lse - ref["lse"]) <= 1e-4 * np.maximum(1.0, np.abs(ref["lse"])))
+    return ref
+
+
+def _decode_run(wl, check_steps, n_sample=8):
+    """Full-size workload: evict once, then decode steps that each append one certain token per
+    unit (pi = 1) and run the certified attention; sampled units are checked end to end against
+    the oracle at `check_steps`."""
+    from paper_2607_21475_amd import cache, ebd_append_certain
+
+    U, n, G = wl.units, wl.context, wl.group
+    budget = wl.budgets[0]
+    _say("full-size %s U=%d n=%d G=%d budget=%s steps=%d" % (wl.name, U, n, G, budget, wl.decode_steps))
+    inp = synth.make_workload_inputs(wl, seed=0, device="cuda")
+    lengths = [n] * U
+    out = cache.evict(inp["K"], inp["V"], inp["scores"], inp["seq_off"], lengths, budget_frac=budget,
+                      n_sink=wl.n_sink, n_recent=wl.n_recent, pi_min=wl.pi_min, seed=0,
+                      extra_rows=wl.decode_steps, want_pi=True)
+    torch.cuda.synchronize()
+    assert not (_np(out.status) & oracle.ST_CAP_OVERFLOW).any()
+    pi_all = _np(out.pi_full)
+    sample = np.sort(np.random.default_rng(1).choice(U, n_sample, replace=False))
+    appended = {int(u): [] for u in sample}
+    ws = None
+    checked = 0
+    for t in range(wl.decode_steps):
+        kn = synth.make_queries(U, 1, seed=10000 + t, device="cuda")[:, 0].contiguous()
+        vn = synth.make_queries(U, 1, seed=20000 + t, device="cuda")[:, 0].contiguous()
+        pos = torch.full((U,), n + t, dtype=torch.int32, device="cuda")
+        ebd_append_certain(U, out.cap_off, out.count, kn, vn, out.Kc, out.Vc, out.pic, out.idxc, pos,
+                           out.status)
+        q = synth.make_queries(U, G, seed=30000 + t, device="cuda")
+        res = cache.attend_certify(out, q, ws=ws)
+        ws = res["ws"]
+        kb, vb = _bits(kn[torch.as_tensor(sample, device="cuda")]), _bits(vn[torch.as_tensor(sample, device="cuda")])
+        for i, u in enumerate(sample):
+            appended[int(u)].append((kb[i], vb[i], n + t))
+        if t in check_steps:
+            torch.cuda.synchronize()
+            assert not (_np(out.status) & oracle.ST_CAP_OVERFLOW).any()
+            for u in sample:
+                sl = slice(int(u) * n, (int(u) + 1) * n)
+                Kc_r, Vc_r, pic_r = _check_unit_end_to_end(
+                    int(u), sl, inp["scores"], inp["K"], inp["V"], pi_all, out, budget, wl.n_sink,
+                    wl.n_recent, wl.pi_min, appended=appended[int(u)])
+                _check_unit_attend(int(u), q, res, Kc_r, Vc_r, pic_r)
+            checked += 1
+            _say("  step %d: %d sampled units match" % (t, len(sample)))
+    assert checked == len(check_steps)
+    del inp, out, res
+    torch.cuda.empty_cache()
+
+
+def test_llama8b_full_size_decode_with_appends():
+    wl = synth.WORKLOADS["llama8b_16k"]
+    _decode_run(wl, check_steps=(0, wl.decode_steps - 1))
+
+
+def test_long_128k_full_size_decode_streamed_scores():
+    """131072-token units: the sampler streams scores (they do not fit the work-group's LDS)."""
+    wl = synth.WORKLOADS["long_128k"]
+    _decode_run(wl, check_steps=(0, wl.decode_steps - 1))
+
+
+def test_replay_grid_chunk_per_unit_budgets():
+    """One chunk of the replay grid: cells cycle through 5 budgets and 3 context lengths, 8 KV
+    heads per cell, G = 1, per-unit budgets; one sampled unit per (budget, context) pair is
+    checked end to end, and the coverage of the radius is reported (not gated)."""
+    from paper_2607_21475_amd import cache
+
+    c0, ncell = 3015, 1512
+    cells = [synth.replay_cell(c) for c in range(c0, c0 + ncell)]
+    H = synth.REPLAY_KV_HEADS
+    lengths = [ctx for (_, ctx, _, _) in cells for _ in range(H)]
+    budgets = [b for (b, _, _, _) in cells for _ in range(H)]
+    U = len(lengths)
+    _say("replay chunk cells %d..%d U=%d rows=%d" % (c0, c0 + ncell, U, sum(lengths)))
+    K, V, seq_off = synth.make_cache(lengths, seed=5, device="cuda")
+    sc = synth.window_scores(K, seq_off, seed=6)
+    q = synth.make_queries(U, 1, seed=7, device="cuda")
+    bpu = torch.tensor(budgets, dtype=torch.float32, device="cuda")
+    out = cache.evict(K, V, sc, seq_off, lengths, budget_per_unit=bpu, seed=9, want_pi=True)
+    res = cache.attend_certify(out, q)
+    torch.cuda.synchronize()
+    assert not (_np(out.status) & oracle.ST_CAP_OVERFLOW).any()
+    pi_all = _np(out.pi_full)
+    off = _np(seq_off)
+    covered = 0
+    for j in range(15):  # cells c0 + j cover every (budget, context) pair once
+        u = j * H + (j % H)
+        sl = slice(int(off[u]), int(off[u + 1]))
+        Kc_r, Vc_r, pic_r = _check_unit_end_to_end(u, sl, sc, K, V, pi_all, out, budgets[u], 4, 64,
+                                                   0.01, seed=9)
+        ref = _check_unit_attend(u, q, res, Kc_r, Vc_r, pic_r)
+        yfull = oracle.full_attention(_bits(q[u]), _bits(K[sl]), _bits(V[sl]))
+        err = np.linalg.norm(ref["y"] - yfull) / np.linalg.norm(yfull)
+        covered += int(err <= ref["r"][0])
+    _say("  radius covered the full-cache output for %d of 15 sampled units" % covered)
