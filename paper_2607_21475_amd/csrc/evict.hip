@@ -12,7 +12,8 @@
 //                 status bits.
 //   evict_copy    one work-group per (unit, block of retained rows): gathers the retained K and
 //                 V rows named by the index list (16 lanes x 16 B per 256-byte row, all loads of
-//                 a thread in flight together).  Evicted rows are never read.
+//                 a thread in flight together, non-temporal loads and stores: every byte is
+//                 touched once).  Evicted rows are never read.
 #include "ebd.h"
 #include "ebd_device.hpp"
 #include "ebd_internal.hpp"
@@ -349,15 +350,15 @@ __global__ __launch_bounds__(kCopyThreads) void evict_copy_kernel(EvictLaunch L)
 #pragma unroll
   for (int k = 0; k < kIter; ++k) {
     const int64_t s = (base + src[k]) * (kHeadDim / 8) + sub;
-    kv[k] = K4[s];
-    vv[k] = V4[s];
+    kv[k] = __builtin_nontemporal_load(&K4[s]);  // streamed once: no cache retention
+    vv[k] = __builtin_nontemporal_load(&V4[s]);
   }
 #pragma unroll
   for (int k = 0; k < kIter; ++k) {
     if (ok[k]) {
       const int64_t d = (cbase + r0 + row + k * kPass) * (kHeadDim / 8) + sub;
-      Kc4[d] = kv[k];
-      Vc4[d] = vv[k];
+      __builtin_nontemporal_store(kv[k], &Kc4[d]);
+      __builtin_nontemporal_store(vv[k], &Vc4[d]);
     }
   }
 }
