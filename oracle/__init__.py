@@ -7,7 +7,8 @@ binding) never imports it and shares no code with it.
 The arithmetic lives in ``ebd_oracle.c`` (plain C, fp64), written from the paper:
   Sec. 3.1 eq. (1) full attention; Sec. 3.3 eq. (2) inclusion probabilities,
   certainty set and Poisson tail; eq. (3) Hajek estimator; Theorem 2 variance
-  estimator; Sec. 3.4 eq. (4) radius.  This module only marshals numpy arrays.
+  estimator; Sec. 3.4 eq. (4) radius; App. "Experimental details" importance
+  scores from accumulated attention.  This module only marshals numpy arrays.
 
 bf16 tensors are passed as their raw uint16 bit patterns.
 """
@@ -74,6 +75,10 @@ def _load():
     lib.ebd_ref_attend_batch.restype = None
     lib.ebd_ref_full_batch.argtypes = [i32, i32, i32, P, P, P, P, f64, P, i32]
     lib.ebd_ref_full_batch.restype = None
+    lib.ebd_ref_window_scores.argtypes = [i64, i32, i32, P, P, P, f64, P]
+    lib.ebd_ref_window_scores.restype = None
+    lib.ebd_ref_window_scores_batch.argtypes = [i32, i32, i32, P, P, P, P, f64, P, i32]
+    lib.ebd_ref_window_scores_batch.restype = None
     lib.ebd_ref_max_threads.argtypes = []
     lib.ebd_ref_max_threads.restype = i32
     _lib = lib
@@ -263,3 +268,39 @@ def full_batch(seq_off, q, K, V, scale=None, nthreads=0):
     _load().ebd_ref_full_batch(U, G, d, _p(seq_off), _p(q), _p(K), _p(V), float(scale), _p(y),
                                int(nthreads))
     return y
+
+
+# --------------------------------------------------------------------------
+# Importance scores (App. "Experimental details", Harness)
+# --------------------------------------------------------------------------
+def window_scores(K, Q, qpos=None, scale=None):
+    """score_i = sum_w softmax_w(scale q_w . k)_i over the keys query w sees (0..qpos[w], or all
+    when qpos is None).  K [n, d], Q [W, d] bf16 bits; returns float64 [n]."""
+    Q = _c(Q, np.uint16)
+    if Q.ndim == 1:
+        Q = Q[None, :]
+    W, d = Q.shape
+    K = _c(K, np.uint16).reshape(-1, d)
+    n = K.shape[0]
+    qp = None if qpos is None else _c(qpos, np.int32)
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.zeros(n, np.float64)
+    _load().ebd_ref_window_scores(n, d, W, _p(K), _p(Q), _p(qp), float(scale), _p(out))
+    return out
+
+
+def window_scores_batch(seq_off, K, Q, qpos=None, scale=None, nthreads=0):
+    """Scores of U units: seq_off [U+1], K [rows, d], Q [U, W, d], qpos [U, W] or None."""
+    off = _c(seq_off, np.int64)
+    U = off.shape[0] - 1
+    Q = _c(Q, np.uint16)
+    W, d = Q.shape[1], Q.shape[2]
+    K = _c(K, np.uint16).reshape(-1, d)
+    qp = None if qpos is None else _c(qpos, np.int32)
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.zeros(int(off[-1]), np.float64)
+    _load().ebd_ref_window_scores_batch(U, d, W, _p(off), _p(K), _p(Q), _p(qp), float(scale),
+                                        _p(out), int(nthreads))
+    return out

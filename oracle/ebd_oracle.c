@@ -15,6 +15,9 @@
  *     Sec. 3.3  Theorem 2  Vhat = Nhat^-2 sum_{S cap T} (1-pi)/pi^2 a^2 |v - yhat|^2
  *     Sec. 3.4  eq. (4)  radius r = (sqrt(2 Vhat ln(1/delta)) + b ln(1/delta)) / (|yhat| + eps0)
  *                        b = max_{S cap T} sqrt((1-pi)/pi^2) a |v - yhat| / Nhat
+ *   App. "Experimental details", Harness: importance scores from accumulated attention
+ *     (strided prefill queries) or an observation window of queries: per query, the
+ *     softmax over the keys it sees, summed over the queries
  *   Counter-based RNG: Philox4x32-10, Salmon, Moraes, Dror & Shaw,
  *     "Parallel random numbers: as easy as 1, 2, 3", SC 2011.
  *
@@ -355,6 +358,42 @@ void ebd_ref_full_attention(int32_t G, int32_t d, int64_t n, const uint16_t *q, 
 }
 
 /* ------------------------------------------------------------------ */
+/* Importance scores (App. "Experimental details", Harness): the       */
+/* attention mass each key receives from a set of queries.  Query w     */
+/* sees keys 0..qpos[w] (a prefill query at position qpos[w]), or every */
+/* key when qpos is NULL (an observation window placed after the        */
+/* cache).  score_i = sum_w softmax_w(scale q_w . k)_i over those keys. */
+/* ------------------------------------------------------------------ */
+void ebd_ref_window_scores(int64_t n, int32_t d, int32_t W, const uint16_t *K, const uint16_t *Q,
+                           const int32_t *qpos, double scale, double *out)
+{
+    double *lg = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    double *qd = (double *)malloc((size_t)d * sizeof(double));
+    for (int64_t i = 0; i < n; ++i) out[i] = 0.0;
+    for (int32_t w = 0; w < W; ++w) {
+        int64_t seen = n;
+        if (qpos) {
+            seen = (int64_t)qpos[w] + 1;
+            if (seen > n) seen = n;
+        }
+        if (seen <= 0) continue;
+        for (int32_t c = 0; c < d; ++c) qd[c] = ref_bf16(Q[(int64_t)w * d + c]);
+        double M = -INFINITY;
+        for (int64_t i = 0; i < seen; ++i) {
+            double dot = 0.0;
+            for (int32_t c = 0; c < d; ++c) dot += qd[c] * ref_bf16(K[i * d + c]);
+            lg[i] = scale * dot;
+            if (lg[i] > M) M = lg[i];
+        }
+        double Z = 0.0;
+        for (int64_t i = 0; i < seen; ++i) Z += exp(lg[i] - M);
+        for (int64_t i = 0; i < seen; ++i) out[i] += exp(lg[i] - M) / Z;
+    }
+    free(lg);
+    free(qd);
+}
+
+/* ------------------------------------------------------------------ */
 /* Batched drivers over independent units (one KV head cache each).   */
 /* Units are independent, so they are split across threads.          */
 /* ------------------------------------------------------------------ */
@@ -449,6 +488,22 @@ void ebd_ref_full_batch(int32_t U, int32_t G, int32_t d, const int64_t *seq_off,
         int64_t base = seq_off[u], n = seq_off[u + 1] - seq_off[u];
         ebd_ref_full_attention(G, d, n, q + (int64_t)u * G * d, K + base * d, V + base * d, scale,
                                y + (int64_t)u * G * d);
+    }
+}
+
+/* Importance scores for U units: Q [U, W, d], qpos [U, W] or NULL, out [rows]. */
+void ebd_ref_window_scores_batch(int32_t U, int32_t d, int32_t W, const int64_t *seq_off,
+                                 const uint16_t *K, const uint16_t *Q, const int32_t *qpos,
+                                 double scale, double *out, int32_t nthreads)
+{
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+    for (int32_t u = 0; u < U; ++u) {
+        int64_t base = seq_off[u], n = seq_off[u + 1] - seq_off[u];
+        ebd_ref_window_scores(n, d, W, K + base * d, Q + (int64_t)u * W * d,
+                              qpos ? qpos + (int64_t)u * W : NULL, scale, out + base);
     }
 }
 
