@@ -116,6 +116,8 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 1 GiB device copy (profiler counter scale)")
+    ap.add_argument("--scores-steps", type=int, default=10,
+                    help="also time the importance-score kernels alone (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate host time for the oracle baseline (0 disables it)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -277,6 +279,39 @@ def main() -> int:
     del src, dst
     roofline["measured_copy_gbs"] = round(2 * (1 << 30) / (best * 1e-3) / 1e9, 1)
 
+    # The step before the path (not part of `value`): importance scores from 32 observation-
+    # window queries per unit, the same recipe as the synthetic inputs' scores, timed alone.
+    imp = None
+    if args.scores_steps > 0:
+        qw = synth.make_queries(U, 32, seed=args.seed + 7, device="cuda")
+        sp_ = ebd.scores_params(U, 32, n, inp["seq_off"])
+        sws = ebd.workspace(ebd.ebd_workspace_size(ebd.EBD_WS_SCORES, sp_))
+        sco = torch.empty_like(inp["scores"])
+        for _ in range(2):
+            ebd.ebd_scores(sp_, qw, inp["K"], sco, sws)
+        torch.cuda.synchronize()
+        ebd.ebd_timing_enable(True)
+        for k in ("scores_stats", "scores_accum"):
+            ebd.ebd_timing_read(k)
+        for _ in range(args.scores_steps):
+            ebd.ebd_scores(sp_, qw, inp["K"], sco, sws)
+        torch.cuda.synchronize()
+        st = {k: ebd.ebd_timing_read(k) for k in ("scores_stats", "scores_accum")}
+        ebd.ebd_timing_enable(False)
+        toks = U * n
+        # each pass reads every cached key once (256 B); the second also writes the score (4 B)
+        sb = {"scores_stats": 256 * toks, "scores_accum": 260 * toks}
+        imp = {"queries_per_unit": 32, "steps": args.scores_steps}
+        tot_ms = 0.0
+        for k, (ms, nl) in st.items():
+            avg = ms / max(nl, 1)
+            tot_ms += ms
+            imp[k] = {"avg_us": round(avg * 1e3, 2), "achieved_gbs": round(sb[k] / (avg * 1e-3) / 1e9, 1),
+                      "frac_hbm": round(sb[k] / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        imp["tokens_per_s"] = round(toks * args.scores_steps / (tot_ms * 1e-3), 1)
+        imp["gbs"] = round(sum(sb.values()) * args.scores_steps / (tot_ms * 1e-3) / 1e9, 1)
+        del qw, sws, sco
+
     # CPU baseline: the fp64 oracle on a bounded sample of the same units, same budgets.
     cpu = None
     if args.cpu_seconds > 0:
@@ -308,6 +343,7 @@ def main() -> int:
         "kernels": kern,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "importance_scores": imp,
         "kernel_sources_hash": kernel_sources_hash(),
     }
     print(json.dumps(line), flush=True)

@@ -171,15 +171,53 @@ ebd_status ebd_append_certain(int32_t num_units, int32_t head_dim, const int64_t
                               const int32_t *pos_new, uint16_t *Kc, uint16_t *Vc, float *pic,
                               int32_t *idxc, uint32_t *status, void *stream);
 
+/*
+ * Importance scores from accumulated attention (App. "Experimental details", Harness: the
+ * sampler's scores come from the attention that prefill queries, or a window of observation
+ * queries, pay to each cached key).  For unit u and its W queries q_w (bf16 [U, W, 128]):
+ *     score_i = sum_w softmax_w(scale q_w . k)_i
+ * where query w sees rows 0 .. qpos[u * W + w] of the unit (a prefill query at that
+ * position; a negative position sees nothing), or every row of the unit when qpos is NULL
+ * (an observation window placed after the cache).  Each query's softmax sums to 1 over the
+ * rows it sees, so the scores of a unit sum to the number of queries that see a row.
+ *   seq_off [U+1] device int64: unit u owns rows seq_off[u] .. seq_off[u+1]-1 of K and of
+ *            `scores` (fp32, written; with EBD_SCORES_ACCUMULATE added to instead, so that
+ *            more than 64 queries can be spread over several calls).
+ *   num_queries W: 1 .. 64.  max_rows >= the longest unit (sizes the split grid; rows of a
+ *   longer unit past the planned splits are neither seen nor written).
+ *   scale: logit scale (0 means 1/sqrt(head_dim)); split_rows: rows per split, one wave
+ *   each (0 = library choice; else a multiple of 16 in [16, 65536]).
+ *   workspace: at least ebd_workspace_size(EBD_WS_SCORES, p) bytes, 256-byte aligned.
+ * Two passes over K: per split, each query's running max and exp-sum; then, with the
+ * unit's combined normalisers, the scores.
+ */
+#define EBD_SCORES_ACCUMULATE 1u
+
+typedef struct ebd_scores_params {
+    int32_t num_units;
+    int32_t head_dim;
+    int32_t num_queries;
+    int32_t split_rows;
+    int64_t max_rows;
+    const int64_t *seq_off;
+    const int32_t *qpos;
+    float scale;
+    uint32_t flags;
+} ebd_scores_params;
+
+ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint16_t *K,
+                      float *scores, void *workspace, size_t ws_bytes, void *stream);
+
 /* which-values for ebd_workspace_size */
 #define EBD_WS_EVICT 0
 #define EBD_WS_ATTEND 1
+#define EBD_WS_SCORES 2
 
 /*
- * Workspace bytes needed by ebd_evict (which = EBD_WS_EVICT, params = ebd_evict_params*)
- * or ebd_attend_certify (EBD_WS_ATTEND, ebd_attend_params*).  Depends only on the host
- * fields of the params (num_units, max_rows, group, split_rows).  Returns 0 on invalid
- * arguments.
+ * Workspace bytes needed by ebd_evict (which = EBD_WS_EVICT, params = ebd_evict_params*),
+ * ebd_attend_certify (EBD_WS_ATTEND, ebd_attend_params*) or ebd_scores (EBD_WS_SCORES,
+ * ebd_scores_params*).  Depends only on the host fields of the params.  Returns 0 on
+ * invalid arguments.
  */
 size_t ebd_workspace_size(int32_t which, const void *params);
 
@@ -193,7 +231,8 @@ const char *ebd_version(void);
  * Kernel timing (profiling aid).  While enabled, every kernel launch of the library is
  * bracketed by HIP events recorded on the launch stream.  ebd_timing_read() waits for the
  * recorded events, and adds the elapsed times of kernel `name` ("evict_select",
- * "evict_copy", "attend_split", "attend_finalize", "append_certain") to *total_ms and
+ * "evict_copy", "attend_split", "attend_finalize", "append_certain", "scores_stats",
+ * "scores_accum") to *total_ms and
  * its launch count to *launches; it then clears that kernel's record.  Not meant for use
  * from several host threads at once.
  */

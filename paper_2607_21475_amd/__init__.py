@@ -41,6 +41,8 @@ EBD_ST_BAD_LAYOUT = 16
 
 EBD_WS_EVICT = 0
 EBD_WS_ATTEND = 1
+EBD_WS_SCORES = 2
+EBD_SCORES_ACCUMULATE = 1
 
 HEAD_DIM = 128
 
@@ -80,12 +82,28 @@ class ebd_attend_params(ctypes.Structure):
     ]
 
 
+class ebd_scores_params(ctypes.Structure):
+    _fields_ = [
+        ("num_units", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("num_queries", ctypes.c_int32),
+        ("split_rows", ctypes.c_int32),
+        ("max_rows", ctypes.c_int64),
+        ("seq_off", ctypes.c_void_p),
+        ("qpos", ctypes.c_void_p),
+        ("scale", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
 _P = ctypes.c_void_p
 _lib.ebd_evict.argtypes = [ctypes.POINTER(ebd_evict_params)] + [_P] * 12 + [ctypes.c_size_t, _P]
 _lib.ebd_evict.restype = ctypes.c_int
 _lib.ebd_attend_certify.argtypes = [ctypes.POINTER(ebd_attend_params)] + [_P] * 11 + \
     [ctypes.c_size_t, _P]
 _lib.ebd_attend_certify.restype = ctypes.c_int
+_lib.ebd_scores.argtypes = [ctypes.POINTER(ebd_scores_params)] + [_P] * 4 + [ctypes.c_size_t, _P]
+_lib.ebd_scores.restype = ctypes.c_int
 _lib.ebd_append_certain.argtypes = [ctypes.c_int32, ctypes.c_int32] + [_P] * 11
 _lib.ebd_append_certain.restype = ctypes.c_int
 _lib.ebd_workspace_size.argtypes = [ctypes.c_int32, _P]
@@ -178,6 +196,21 @@ def attend_params(num_units, group, max_rows, cap_off, split_rows=0, scale=0.0, 
     return p
 
 
+def scores_params(num_units, num_queries, max_rows, seq_off, qpos=None, split_rows=0, scale=0.0,
+                  accumulate=False) -> ebd_scores_params:
+    p = ebd_scores_params()
+    p.num_units = int(num_units)
+    p.head_dim = HEAD_DIM
+    p.num_queries = int(num_queries)
+    p.split_rows = int(split_rows)
+    p.max_rows = int(max_rows)
+    p.seq_off = _ptr(seq_off, torch.int64, "seq_off")
+    p.qpos = _ptr(qpos, torch.int32, "qpos")
+    p.scale = float(scale)
+    p.flags = EBD_SCORES_ACCUMULATE if accumulate else 0
+    return p
+
+
 def ebd_workspace_size(which: int, params) -> int:
     n = _lib.ebd_workspace_size(int(which), ctypes.byref(params))
     if n == 0 and params.num_units > 0:
@@ -213,6 +246,15 @@ def ebd_attend_certify(params: ebd_attend_params, q, Kc, Vc, pic, count, y, vhat
                                    _ptr(workspace, None, "workspace"),
                                    workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ebd_attend_certify", code)
+
+
+def ebd_scores(params: ebd_scores_params, q, K, scores, workspace, stream=None) -> None:
+    """Launch the importance-score passes (asynchronous on the current stream)."""
+    bf = torch.bfloat16
+    code = _lib.ebd_scores(ctypes.byref(params), _ptr(q, bf, "q"), _ptr(K, bf, "K"),
+                           _ptr(scores, torch.float32, "scores"), _ptr(workspace, None, "workspace"),
+                           workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("ebd_scores", code)
 
 
 def ebd_append_certain(num_units, cap_off, count, k_new, v_new, Kc, Vc, pic, idxc=None,

@@ -11,8 +11,9 @@ from typing import Optional, Sequence, Union
 
 import torch
 
-from . import (EBD_WS_ATTEND, EBD_WS_EVICT, HEAD_DIM, attend_params, ebd_attend_certify,
-               ebd_evict, ebd_workspace_size, evict_params, workspace)
+from . import (EBD_WS_ATTEND, EBD_WS_EVICT, EBD_WS_SCORES, HEAD_DIM, attend_params,
+               ebd_attend_certify, ebd_evict, ebd_scores, ebd_workspace_size, evict_params,
+               scores_params, workspace)
 
 
 def unit_capacity(n: int, budget_frac: float, n_prot: int, extra: int = 0, align: int = 16) -> int:
@@ -115,6 +116,24 @@ def attend_certify(cache: RetainedCache, q: torch.Tensor, split_rows: int = 0, d
     ebd_attend_certify(p, q, cache.Kc, cache.Vc, cache.pic, cache.count, y, vhat, lse, ws,
                        brange=b, radius=r)
     return {"y": y, "vhat": vhat, "lse": lse, "b": b, "r": r, "ws": ws}
+
+
+def importance_scores(K: torch.Tensor, seq_off: torch.Tensor, q: torch.Tensor, max_rows: int,
+                      qpos: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+                      accumulate: bool = False, split_rows: int = 0, scale: float = 0.0,
+                      ws: Optional[torch.Tensor] = None):
+    """Attention mass each cached key receives from the queries q [U, W, 128] (W <= 64 per
+    call; more queries: further calls with accumulate=True).  Returns (scores fp32, workspace)."""
+    U, W, _ = q.shape
+    dev = K.device
+    p = scores_params(U, W, max_rows, seq_off, qpos, split_rows, scale, accumulate)
+    need = ebd_workspace_size(EBD_WS_SCORES, p)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    if scores is None:
+        scores = torch.empty((max(K.shape[0], 1),), dtype=torch.float32, device=dev)
+    ebd_scores(p, q, K, scores, ws)
+    return scores, ws
 
 
 def rescans(ws: torch.Tensor, num_units: int, group: int) -> int:

@@ -35,13 +35,6 @@ namespace ebd {
 
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
-__device__ __forceinline__ float fast_sqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
-
 __device__ __forceinline__ float scale_of(float mw, float M) {
   return (mw == -INFINITY) ? 0.0f : fast_exp2(mw - M);
 }
@@ -50,16 +43,6 @@ __device__ __forceinline__ float scale_of(float mw, float M) {
 __device__ __forceinline__ uint32_t bf16_up(float x) {
   const uint32_t b = __float_as_uint(x);
   return (b >> 16) + ((b & 0xffffu) ? 1u : 0u);
-}
-
-// Buffer resources (gfx9 raw buffers: stride 0, range checked per access).  Loads at or beyond
-// the range return zeros without touching memory, so a split's tail tiles and the prefetches past
-// its end need no clamping.
-constexpr int kRsrcWord3 = 0x00020000;  // 32-bit data format, untyped access
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t nbytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)nbytes,
-                                           kRsrcWord3);
 }
 
 struct Tile {

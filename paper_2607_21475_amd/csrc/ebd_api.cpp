@@ -101,6 +101,35 @@ int32_t attend_nsplit(const ebd_attend_params *p, int32_t sr) {
   return (int32_t)(ns > 0 ? ns : 1);
 }
 
+// Rows per scores split: as for attention, one split per unit when the units give enough
+// waves, else equal splits (at least 256 rows, at most 8192).
+int32_t scores_split_rows(const ebd_scores_params *p) {
+  if (p->split_rows > 0) return p->split_rows;
+  const int64_t n = p->max_rows > 0 ? p->max_rows : 1;
+  const int64_t U = p->num_units > 0 ? p->num_units : 1;
+  int64_t ns = (kSplitWaves + U - 1) / U;
+  ns = std::max<int64_t>(ns, (n + 8191) / 8192);
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, n / 256));
+  return (int32_t)(((n + ns - 1) / ns + 15) / 16 * 16);
+}
+
+int32_t scores_nsplit(const ebd_scores_params *p, int32_t sr) {
+  const int64_t ns = (p->max_rows + sr - 1) / sr;
+  return (int32_t)(ns > 0 ? ns : 1);
+}
+
+bool valid_scores_params(const ebd_scores_params *p) {
+  if (!p) return false;
+  if (p->num_units < 0 || p->max_rows < 0 || p->max_rows > ((int64_t)1 << 31)) return false;
+  if (p->num_queries < 1 || p->num_queries > kScoresMaxQueries) return false;
+  if (p->num_units > 0 && !p->seq_off) return false;
+  if (p->split_rows != 0 && (p->split_rows < 16 || p->split_rows > 65536 || p->split_rows % 16))
+    return false;
+  if ((p->flags & ~EBD_SCORES_ACCUMULATE) != 0u) return false;
+  if (p->scale < 0.0f || !std::isfinite(p->scale)) return false;
+  return true;
+}
+
 bool valid_evict_params(const ebd_evict_params *p) {
   if (!p) return false;
   if (p->num_units < 0 || p->max_rows < 0 || p->max_rows > ((int64_t)1 << 31)) return false;
@@ -156,6 +185,12 @@ size_t ebd_workspace_size(int32_t which, const void *params) {
     if (!valid_attend_params(p)) return 0;
     const int32_t sr = attend_split_rows(p);
     return attend_workspace_bytes(p->num_units, attend_nsplit(p, sr), p->group, sr);
+  }
+  if (which == EBD_WS_SCORES) {
+    const ebd_scores_params *p = static_cast<const ebd_scores_params *>(params);
+    if (!valid_scores_params(p)) return 0;
+    const int32_t sr = scores_split_rows(p);
+    return scores_workspace_bytes(p->num_units, scores_nsplit(p, sr), p->num_queries);
   }
   return 0;
 }
@@ -261,6 +296,41 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
     return EBD_ERR_HIP;
   if (L.nsplit > 1 &&
       timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  return EBD_OK;
+}
+
+ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint16_t *K,
+                      float *scores, void *workspace, size_t ws_bytes, void *stream) {
+  if (!valid_scores_params(p)) return EBD_ERR_INVALID_ARG;
+  if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  if (p->num_units == 0) return EBD_OK;
+  if (!q || !K || !scores) return EBD_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(scores, 4)) return EBD_ERR_INVALID_ARG;
+  const int32_t sr = scores_split_rows(p);
+  const int32_t nsplit = scores_nsplit(p, sr);
+  const size_t need = scores_workspace_bytes(p->num_units, nsplit, p->num_queries);
+  if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
+  const ebd_status ds = check_device();
+  if (ds != EBD_OK) return ds;
+
+  ScoresLaunch L;
+  L.U = p->num_units;
+  L.W = p->num_queries;
+  L.nsplit = nsplit;
+  L.split_rows = sr;
+  L.seq_off = p->seq_off;
+  L.qpos = p->qpos;
+  L.q = q;
+  L.K = K;
+  L.scale = p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)kHeadDim);
+  L.flags = p->flags;
+  L.scores = scores;
+  L.stats = static_cast<float2 *>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (timed("scores_stats", s, [&] { return launch_scores_stats(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  if (timed("scores_accum", s, [&] { return launch_scores_accum(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
   return EBD_OK;
 }

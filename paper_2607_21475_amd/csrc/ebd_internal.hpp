@@ -19,6 +19,7 @@ constexpr int kSplitMaxRows = 4096;  // default split length cap (bounds the lau
 constexpr int kSplitMinRows = 256;   // default split length floor
 constexpr int kSplitWaves = 1536;    // default: cut units until the launch has this many waves
 constexpr int kSplitRowsLimit = 8192;  // largest split a caller may ask for (LDS of one wave)
+constexpr int kScoresMaxQueries = 64;  // queries per ebd_scores call (four MFMA blocks)
 constexpr int kChunkRows = 512;      // range-term candidates are kept per chunk of a split
 constexpr int kCand = 32;            // candidates per (chunk, head)
 
@@ -95,12 +96,26 @@ struct AppendLaunch {
   uint32_t *status;
 };
 
+struct ScoresLaunch {
+  int32_t U, W, nsplit, split_rows;
+  const int64_t *seq_off;
+  const int32_t *qpos;  // [U, W] last row each query sees, or NULL (every row)
+  const uint16_t *q, *K;
+  float scale;
+  uint32_t flags;
+  float *scores;
+  float2 *stats;        // [U, nsplit, W] (max, exp-sum) per split and query
+};
+
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows);
+size_t scores_workspace_bytes(int32_t U, int32_t nsplit, int32_t W);
 
 hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s);
 hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s);
 hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_attend_finalize(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_append_certain(const AppendLaunch &L, hipStream_t s);
+hipError_t launch_scores_stats(const ScoresLaunch &L, hipStream_t s);
+hipError_t launch_scores_accum(const ScoresLaunch &L, hipStream_t s);
 
 }  // namespace ebd

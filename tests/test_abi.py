@@ -20,8 +20,9 @@ def _declared_functions():
 
 def test_header_declares_the_boundary():
     names = _declared_functions()
-    for fn in ("ebd_evict", "ebd_attend_certify", "ebd_append_certain", "ebd_workspace_size",
-               "ebd_status_string", "ebd_version", "ebd_timing_enable", "ebd_timing_read"):
+    for fn in ("ebd_evict", "ebd_attend_certify", "ebd_append_certain", "ebd_scores",
+               "ebd_workspace_size", "ebd_status_string", "ebd_version", "ebd_timing_enable",
+               "ebd_timing_read"):
         assert fn in names, fn
 
 
@@ -151,6 +152,45 @@ def test_workspace_sizes():
         a.split_rows = bad
         assert lib.ebd_workspace_size(ebd.EBD_WS_ATTEND, ctypes.byref(a)) == 0
     assert lib.ebd_workspace_size(7, ctypes.byref(a)) == 0
+
+
+def test_scores_argument_validation_and_workspace():
+    ebd, lib = _lib()
+
+    def params(**kw):
+        p = ebd.ebd_scores_params()
+        p.num_units = kw.get("U", 4)
+        p.head_dim = kw.get("d", 128)
+        p.num_queries = kw.get("W", 32)
+        p.split_rows = kw.get("split", 0)
+        p.max_rows = kw.get("max_rows", 6144)
+        p.seq_off = FAKE
+        p.flags = kw.get("flags", 0)
+        return p
+
+    def call(p, ws=FAKE, ws_bytes=1 << 30):
+        return lib.ebd_scores(ctypes.byref(p), FAKE, FAKE, FAKE, ws, ws_bytes, None)
+
+    assert call(params(d=64)) == ebd.EBD_ERR_UNSUPPORTED
+    for bad in (dict(W=0), dict(W=65), dict(split=40), dict(split=65552), dict(flags=2),
+                dict(U=-1), dict(max_rows=-1)):
+        assert call(params(**bad)) == ebd.EBD_ERR_INVALID_ARG, bad
+    assert call(params(), ws_bytes=64) == ebd.EBD_ERR_WORKSPACE
+    assert call(params(), ws=FAKE + 16) == ebd.EBD_ERR_WORKSPACE
+    assert call(params(U=0)) == ebd.EBD_OK
+    assert lib.ebd_scores(None, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == ebd.EBD_ERR_INVALID_ARG
+
+    def ws(U, nsplit, W):  # (max, exp-sum) per (unit, split, query), 256-byte padded
+        return (8 * U * nsplit * W + 255) // 256 * 256
+
+    p = params(U=1792, W=32, max_rows=6144)  # enough units: one split each
+    assert lib.ebd_workspace_size(ebd.EBD_WS_SCORES, ctypes.byref(p)) == ws(1792, 1, 32)
+    p = params(U=1024, W=64, max_rows=131072)  # long units: splits of at most 8192 rows
+    assert lib.ebd_workspace_size(ebd.EBD_WS_SCORES, ctypes.byref(p)) == ws(1024, 16, 64)
+    p = params(U=8, W=7, max_rows=4096)  # few units: 256-row splits
+    assert lib.ebd_workspace_size(ebd.EBD_WS_SCORES, ctypes.byref(p)) == ws(8, 16, 7)
+    p = params(U=8, W=7, max_rows=4096, split=48)
+    assert lib.ebd_workspace_size(ebd.EBD_WS_SCORES, ctypes.byref(p)) == ws(8, 86, 7)
 
 
 def test_binding_requires_gpu_tensors():
