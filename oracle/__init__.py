@@ -30,6 +30,11 @@ ST_BUDGET_FLOOR = 2
 ST_NO_EVICTION = 4
 ST_BAD_SCORE = 8
 
+DESIGN_POISSON = 0
+DESIGN_SYSTEMATIC = 1
+DESIGN_TOPK = 2
+DESIGN_UNIFORM = 3
+
 
 def build(force: bool = True) -> str:
     """Compile ebd_oracle.c with gcc into libebd_oracle.so (no fast-math)."""
@@ -68,7 +73,13 @@ def _load():
     lib.ebd_ref_full_attention.argtypes = [i32, i32, i64, P, P, P, f64, P]
     lib.ebd_ref_full_attention.restype = None
     lib.ebd_ref_evict_batch.argtypes = [i32, i32, P, P, P, P, P, i32, i32, f64, P, f64, u64, P, u32,
-                                        i32, P, P, P, P, P, P, P, P, P, i32]
+                                        i32, i32, P, P, P, P, P, P, P, P, P, i32]
+    lib.ebd_ref_systematic_start.argtypes = [u64, u32, u32]
+    lib.ebd_ref_systematic_start.restype = u32
+    lib.ebd_ref_mask_systematic.argtypes = [i64, P, u64, u32, u32, P]
+    lib.ebd_ref_mask_systematic.restype = i64
+    lib.ebd_ref_topk_probs.argtypes = [i64, P, i32, i32, f64, P]
+    lib.ebd_ref_topk_probs.restype = u32
     lib.ebd_ref_evict_batch.restype = None
     lib.ebd_ref_attend_batch.argtypes = [i32, i32, i32, P, P, P, P, P, P, f64, f64, f64, i32,
                                          P, P, P, P, P, i32]
@@ -133,6 +144,27 @@ def mask(pi32, seed, unit, epoch=0):
     return m[: p.shape[0]]
 
 
+def systematic_start(seed: int, unit: int, epoch: int = 0) -> int:
+    return int(_load().ebd_ref_systematic_start(seed, unit, epoch))
+
+
+def mask_systematic(pi32, seed, unit, epoch=0):
+    """Fixed-size systematic design at the stored pi (one start per unit)."""
+    p = _c(pi32, np.float32)
+    m = np.zeros(max(p.shape[0], 1), np.uint8)
+    _load().ebd_ref_mask_systematic(p.shape[0], _p(p), seed, unit, epoch, _p(m))
+    return m[: p.shape[0]]
+
+
+def topk_probs(scores, n_sink, n_recent, budget_frac):
+    """Deterministic top-k comparison design: pi in {0, 1}; returns (pi, status)."""
+    s = _c(scores, np.float32)
+    n = s.shape[0]
+    pi = np.zeros(max(n, 1), np.float64)
+    st = _load().ebd_ref_topk_probs(n, _p(s), n_sink, n_recent, float(budget_frac), _p(pi))
+    return pi[:n], int(st)
+
+
 def compact(msk, pi32, K, V, cap=None):
     """Stable compaction. K, V uint16 [n, d]. Returns (Kc, Vc, pic, idx, count)."""
     msk = _c(msk, np.uint8)
@@ -194,7 +226,7 @@ def full_attention(q, K, V, scale=None):
 # --------------------------------------------------------------------------
 def evict_batch(seq_off, cap_off, scores, K, V, n_sink, n_recent, budget_frac=0.1,
                 budget_per_unit=None, pi_min=0.01, seed=0, seed_per_unit=None, epoch=0,
-                pi_mode=0, pi_given=None, nthreads=0):
+                pi_mode=0, pi_given=None, design=0, nthreads=0):
     seq_off = _c(seq_off, np.int64)
     cap_off = _c(cap_off, np.int64)
     U = seq_off.shape[0] - 1
@@ -219,7 +251,7 @@ def evict_batch(seq_off, cap_off, scores, K, V, n_sink, n_recent, budget_frac=0.
     }
     _load().ebd_ref_evict_batch(U, d, _p(seq_off), _p(cap_off), _p(scores), _p(K), _p(V), n_sink,
                                 n_recent, float(budget_frac), _p(bpu), float(pi_min), int(seed),
-                                _p(spu), int(epoch), int(pi_mode), _p(pg), _p(out["Kc"]),
+                                _p(spu), int(epoch), int(pi_mode), int(design), _p(pg), _p(out["Kc"]),
                                 _p(out["Vc"]), _p(out["pic"]), _p(out["idx"]), _p(out["count"]),
                                 _p(out["lambda"]), _p(out["pi_full"]), _p(out["status"]),
                                 int(nthreads))

@@ -33,6 +33,14 @@
  *   - Retained tokens keep ascending original order.
  *   - The offset -ln(pi) applies to every retained token (0 when pi = 1).
  *
+ *   - Fixed-size systematic design: integer weights a_i = ceil(pi32_i 2^32) (the
+ *     Poisson test's exact inclusion probability), cumulative sums C_i, start
+ *     u = word 0 of Philox4x32-10(counter = (0, u, epoch, 0x45424453), key = seed);
+ *     position i is kept iff a point u + k 2^32 falls in [C_{i-1}, C_i).
+ *   - Top-k comparison design: the protected positions and the k = floor(m + 1/2)
+ *     largest cleaned tail scores, ties to the lower position, kept with pi = 1.
+ *   - Uniform comparison design: every tail score taken as 1 (pi = clip(m/|T|, eps, 1)).
+ *
  * Everything is fp64 except the stored per-token pi, which is rounded once to
  * fp32 (the stored design), exactly as the library stores it.
  */
@@ -49,7 +57,15 @@
 #define REF_ST_NO_EVICTION 4u
 #define REF_ST_BAD_SCORE 8u
 
-#define REF_PHILOX_TAG 0x45424431u /* "EBD1" */
+#define REF_PHILOX_TAG 0x45424431u     /* "EBD1": the per-token Poisson stream */
+#define REF_SYSTEMATIC_TAG 0x45424453u /* "EBDS": the per-unit systematic start */
+
+/* Sampling designs (Sec. 3.3 Poisson; App. "Experimental details": fixed-size systematic
+   sampling at the same pi; the deterministic top-k and uniform comparison arms). */
+#define REF_DESIGN_POISSON 0
+#define REF_DESIGN_SYSTEMATIC 1
+#define REF_DESIGN_TOPK 2
+#define REF_DESIGN_UNIFORM 3
 
 /* ------------------------------------------------------------------ */
 /* bf16 bits -> double (exact: bf16 is the top half of an fp32)        */
@@ -221,6 +237,102 @@ int64_t ebd_ref_mask(int64_t n, const float *pi32, uint64_t seed, uint32_t unit,
         kept += mask[i];
     }
     return kept;
+}
+
+/* ------------------------------------------------------------------ */
+/* Fixed-size systematic sampling at the same inclusion probabilities  */
+/* (App. "Experimental details"; Hajek 1964): one uniform start per    */
+/* unit, points u + k 2^32 on the cumulative integer weights.          */
+/* ------------------------------------------------------------------ */
+uint32_t ebd_ref_systematic_start(uint64_t seed, uint32_t unit, uint32_t epoch)
+{
+    const uint32_t ctr[4] = {0u, unit, epoch, REF_SYSTEMATIC_TAG};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    ebd_ref_philox4x32_10(ctr, key, out);
+    return out[0];
+}
+
+/* Number of points u + k 2^32 (k >= 0) strictly below C. */
+static uint64_t ref_points_below(uint64_t C, uint32_t u)
+{
+    return C > (uint64_t)u ? ((C - (uint64_t)u - 1u) >> 32) + 1u : 0u;
+}
+
+int64_t ebd_ref_mask_systematic(int64_t n, const float *pi32, uint64_t seed, uint32_t unit,
+                                uint32_t epoch, uint8_t *mask)
+{
+    const uint32_t u = ebd_ref_systematic_start(seed, unit, epoch);
+    uint64_t C = 0;
+    int64_t kept = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        /* pi32 * 2^32 is exact in fp64; its ceiling is the Poisson test's integer threshold */
+        const uint64_t a = (uint64_t)ceil((double)pi32[i] * 4294967296.0);
+        const uint64_t Cn = C + a;
+        mask[i] = (uint8_t)(ref_points_below(Cn, u) - ref_points_below(C, u));
+        kept += mask[i];
+        C = Cn;
+    }
+    return kept;
+}
+
+/* ------------------------------------------------------------------ */
+/* Comparison designs: deterministic top-k and uniform tail sampling.  */
+/* ------------------------------------------------------------------ */
+static const double *ref_sort_scores;
+static int ref_by_score_desc(const void *x, const void *y)
+{
+    int64_t i = *(const int64_t *)x, j = *(const int64_t *)y;
+    double a = ref_sort_scores[i], b = ref_sort_scores[j];
+    if (a > b) return -1;
+    if (a < b) return 1;
+    return i < j ? -1 : (i > j ? 1 : 0);
+}
+
+/* Top-k: pi = 1 on P and on the k = floor(m + 1/2) best tail positions, 0 elsewhere. */
+uint32_t ebd_ref_topk_probs(int64_t n, const float *scores, int32_t n_sink, int32_t n_recent,
+                            double budget_frac, double *pi_out)
+{
+    uint32_t status = 0;
+    double *s = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    int64_t *idx = (int64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    int64_t n_tail = 0, n_prot = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        double v = (double)scores[i];
+        if (!isfinite(v) || v < 0.0) {
+            status |= REF_ST_BAD_SCORE;
+            v = 0.0;
+        }
+        s[i] = v;
+        if (ref_is_protected(i, n, n_sink, n_recent)) {
+            pi_out[i] = 1.0;
+            n_prot++;
+        } else {
+            pi_out[i] = 0.0;
+            idx[n_tail++] = i;
+        }
+    }
+    double m = budget_frac * (double)n - (double)n_prot;
+    int64_t k = (int64_t)floor(m + 0.5);
+    if (k < 0) k = 0;
+    if (k >= n_tail) {
+        k = n_tail;
+        if (n_tail > 0) status |= REF_ST_NO_EVICTION;
+    }
+    /* qsort is not reentrant with a file-scope key: callers run one unit per thread, so the
+       sort is done under a critical section */
+#ifdef _OPENMP
+#pragma omp critical(ref_topk_sort)
+#endif
+    {
+        ref_sort_scores = s;
+        qsort(idx, (size_t)n_tail, sizeof(int64_t), ref_by_score_desc);
+        ref_sort_scores = NULL;
+    }
+    for (int64_t r = 0; r < k; ++r) pi_out[idx[r]] = 1.0;
+    free(s);
+    free(idx);
+    return status;
 }
 
 /*
@@ -413,7 +525,7 @@ void ebd_ref_evict_batch(int32_t U, int32_t d, const int64_t *seq_off, const int
                          int32_t n_sink, int32_t n_recent, double budget_frac,
                          const float *budget_per_unit, double pi_min, uint64_t seed,
                          const uint64_t *seed_per_unit, uint32_t epoch, int32_t pi_mode,
-                         const float *pi_given,
+                         int32_t design, const float *pi_given,
                          uint16_t *Kc, uint16_t *Vc, float *pic, int32_t *idxc, int32_t *count,
                          double *lambda_out, float *pi_full, uint32_t *status, int32_t nthreads)
 {
@@ -433,12 +545,25 @@ void ebd_ref_evict_batch(int32_t U, int32_t d, const int64_t *seq_off, const int
             memcpy(pi32, pi_given + base, (size_t)n * sizeof(float));
         } else {
             double f = budget_per_unit ? (double)budget_per_unit[u] : budget_frac;
-            st = ebd_ref_inclusion_probs(n, scores + base, n_sink, n_recent, f, pi_min, pi_mode,
-                                         &lam, pi64);
+            if (design == REF_DESIGN_TOPK) {
+                st = ebd_ref_topk_probs(n, scores + base, n_sink, n_recent, f, pi64);
+            } else if (design == REF_DESIGN_UNIFORM) {
+                float *ones = (float *)malloc((size_t)(n > 0 ? n : 1) * sizeof(float));
+                for (int64_t i = 0; i < n; ++i) ones[i] = 1.0f;
+                st = ebd_ref_inclusion_probs(n, ones, n_sink, n_recent, f, pi_min, pi_mode, &lam,
+                                             pi64);
+                free(ones);
+            } else {
+                st = ebd_ref_inclusion_probs(n, scores + base, n_sink, n_recent, f, pi_min,
+                                             pi_mode, &lam, pi64);
+            }
             for (int64_t i = 0; i < n; ++i) pi32[i] = (float)pi64[i];
         }
         uint64_t sd = seed_per_unit ? seed_per_unit[u] : seed;
-        ebd_ref_mask(n, pi32, sd, (uint32_t)u, epoch, mask);
+        if (design == REF_DESIGN_SYSTEMATIC)
+            ebd_ref_mask_systematic(n, pi32, sd, (uint32_t)u, epoch, mask);
+        else
+            ebd_ref_mask(n, pi32, sd, (uint32_t)u, epoch, mask);
         int64_t kept = ebd_ref_compact(n, d, mask, pi32, K + base * d, V + base * d, cap,
                                        Kc + cbase * d, Vc + cbase * d, pic + cbase, idxc + cbase);
         if (kept > cap) st |= REF_ST_CAP_OVERFLOW;
