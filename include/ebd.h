@@ -74,7 +74,23 @@ typedef enum ebd_status {
  *   seed, seed_per_unit [U] (device or NULL), epoch: the Philox4x32-10 stream.  Token i of
  *            unit u is kept iff x < pi_i * 2^32, x = word (i mod 4) of
  *            Philox4x32-10(counter = (i/4, u, epoch, 0x45424431), key = (seed lo, seed hi)).
+ *   design   EBD_DESIGN_POISSON (0, Sec. 3.3): independent retention as above.
+ *            EBD_DESIGN_SYSTEMATIC (1, App. "Experimental details", fixed-size systematic
+ *            sampling at the same pi): integer weights a_i = ceil(pi_i 2^32), cumulative sums
+ *            C_i over the unit, one start s = word 0 of Philox4x32-10(counter = (0, u, epoch,
+ *            0x45424453), key = seed); position i is kept iff a point s + k 2^32 (k >= 0) lies
+ *            in [C_{i-1}, C_i).  The retained size is floor or ceil of sum_i a_i / 2^32.
+ *            EBD_DESIGN_TOPK (2, the deterministic comparison arm): the protected positions
+ *            and the k = floor(m + 1/2) largest tail scores (ties to the lower position), all
+ *            with pi = 1; other positions get pi = 0; lambda_out is 0.
+ *            EBD_DESIGN_UNIFORM (3, the uniform comparison arm): every tail score is taken
+ *            as 1 (scores are not read), so pi = clip(m / |T|, eps, 1) on the tail.
  */
+#define EBD_DESIGN_POISSON 0
+#define EBD_DESIGN_SYSTEMATIC 1
+#define EBD_DESIGN_TOPK 2
+#define EBD_DESIGN_UNIFORM 3
+
 typedef struct ebd_evict_params {
     int32_t num_units;
     int32_t head_dim;
@@ -91,10 +107,11 @@ typedef struct ebd_evict_params {
     uint64_t seed;
     const uint64_t *seed_per_unit;
     uint32_t epoch;
+    int32_t design;
 } ebd_evict_params;
 
 /*
- * ebd_evict -- the Poisson tail sampler for U units (Sec. 3.3; Sec. 3.1 for deletion).
+ * ebd_evict -- the tail sampler for U units (Sec. 3.3; Sec. 3.1 for deletion).
  *   scores [rows] fp32 importance (input of eq. (2)); K, V [rows, 128] bf16.
  *   Outputs (compacted, stable: ascending original position):
  *     Kc, Vc [cap rows, 128] bf16   retained rows

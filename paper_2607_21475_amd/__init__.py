@@ -39,6 +39,11 @@ EBD_ST_NO_EVICTION = 4
 EBD_ST_BAD_SCORE = 8
 EBD_ST_BAD_LAYOUT = 16
 
+EBD_DESIGN_POISSON = 0
+EBD_DESIGN_SYSTEMATIC = 1
+EBD_DESIGN_TOPK = 2
+EBD_DESIGN_UNIFORM = 3
+
 EBD_WS_EVICT = 0
 EBD_WS_ATTEND = 1
 EBD_WS_SCORES = 2
@@ -64,6 +69,7 @@ class ebd_evict_params(ctypes.Structure):
         ("seed", ctypes.c_uint64),
         ("seed_per_unit", ctypes.c_void_p),
         ("epoch", ctypes.c_uint32),
+        ("design", ctypes.c_int32),
     ]
 
 
@@ -160,7 +166,7 @@ def ebd_version() -> str:
 
 def evict_params(num_units, max_rows, max_capacity, seq_off, cap_off, n_sink=4, n_recent=64,
                  budget_frac=0.1, budget_per_unit=None, pi_min=0.01, pi_mode=0, seed=0,
-                 seed_per_unit=None, epoch=0) -> ebd_evict_params:
+                 seed_per_unit=None, epoch=0, design=0) -> ebd_evict_params:
     p = ebd_evict_params()
     p.num_units = int(num_units)
     p.head_dim = HEAD_DIM
@@ -177,6 +183,7 @@ def evict_params(num_units, max_rows, max_capacity, seq_off, cap_off, n_sink=4, 
     p.seed = int(seed) & 0xFFFFFFFFFFFFFFFF
     p.seed_per_unit = _ptr(seed_per_unit, torch.int64, "seed_per_unit")
     p.epoch = int(epoch) & 0xFFFFFFFF
+    p.design = int(design)
     return p
 
 

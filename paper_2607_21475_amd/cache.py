@@ -68,7 +68,7 @@ def evict(K: torch.Tensor, V: torch.Tensor, scores: torch.Tensor, seq_off: torch
           lengths: Sequence[int], budget_frac: float = 0.1, budget_per_unit=None,
           n_sink: int = 4, n_recent: int = 64, pi_min: float = 0.01, pi_mode: int = 0,
           seed: int = 0, seed_per_unit=None, epoch: int = 0, extra_rows: int = 0,
-          want_pi: bool = False, cap_off_host=None) -> RetainedCache:
+          want_pi: bool = False, cap_off_host=None, design: int = 0) -> RetainedCache:
     dev = K.device
     U = len(lengths)
     if cap_off_host is None:
@@ -91,7 +91,7 @@ def evict(K: torch.Tensor, V: torch.Tensor, scores: torch.Tensor, seq_off: torch
     )
     p = evict_params(U, max(lengths) if lengths else 0, out.max_cap, seq_off, cap_off, n_sink,
                      n_recent, budget_frac, budget_per_unit, pi_min, pi_mode, seed, seed_per_unit,
-                     epoch)
+                     epoch, design)
     ws = workspace(ebd_workspace_size(EBD_WS_EVICT, p), dev)
     ebd_evict(p, scores, K, V, out.Kc, out.Vc, out.pic, out.idxc, out.count, out.status, ws,
               lambda_out=out.lam, pi_full=out.pi_full)

@@ -138,6 +138,7 @@ bool valid_evict_params(const ebd_evict_params *p) {
   if (p->n_sink < 0 || p->n_recent < 0) return false;
   if (!(p->pi_min > 0.0f && p->pi_min <= 1.0f)) return false;
   if (p->pi_mode != 0 && p->pi_mode != 1) return false;
+  if (p->design < EBD_DESIGN_POISSON || p->design > EBD_DESIGN_UNIFORM) return false;
   if (!p->budget_per_unit && !std::isfinite(p->budget_frac)) return false;
   return true;
 }
@@ -224,6 +225,7 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
   L.budget_per_unit = p->budget_per_unit;
   L.pi_min = p->pi_min;
   L.pi_mode = p->pi_mode;
+  L.design = p->design;
   L.seed = p->seed;
   L.seed_per_unit = p->seed_per_unit;
   L.epoch = p->epoch;

@@ -6,7 +6,8 @@
 
 namespace ebd {
 
-constexpr uint32_t kPhiloxTag = 0x45424431u;  // "EBD1": fourth counter word of the mask stream
+constexpr uint32_t kPhiloxTag = 0x45424431u;      // "EBD1": fourth counter word of the mask stream
+constexpr uint32_t kSystematicTag = 0x45424453u;  // "EBDS": ... of the systematic start
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));

@@ -57,6 +57,7 @@ struct EvictLaunch {
   const float *budget_per_unit;
   float pi_min;
   int32_t pi_mode;
+  int32_t design;  // EBD_DESIGN_*
   uint64_t seed;
   const uint64_t *seed_per_unit;
   uint32_t epoch;

@@ -6,10 +6,12 @@
 //                 16384 tokens, protected positions marked by a negative sentinel; longer units
 //                 are re-read from memory), solves lambda with sum_T clip(lambda s, eps, 1) = m by
 //                 safeguarded Newton steps on the piecewise linear g(lambda) (exact once the
-//                 piece is found), then walks the unit in 1024-token blocks: Philox words, exact
-//                 retention test, ballot ranks plus a cross-wave prefix, and writes the stored pi
-//                 and original position of every retained row in order, plus the count and the
-//                 status bits.
+//                 piece is found), then walks the unit in 1024-token blocks: Philox words and the
+//                 exact retention test (Poisson), or a block scan of the integer weights
+//                 ceil(pi 2^32) against one start per unit (fixed-size systematic design), or
+//                 the score threshold of a radix select (top-k comparison design); ballot ranks
+//                 plus a cross-wave prefix give the order in which the stored pi and original
+//                 position of every retained row are written, plus the count and status bits.
 //   evict_copy    one work-group per (unit, block of retained rows): gathers the retained K and
 //                 V rows named by the index list (16 lanes x 16 B per 256-byte row, all loads of
 //                 a thread in flight together, non-temporal loads and stores: every byte is
@@ -28,7 +30,7 @@ __device__ __forceinline__ float clean_score(float s, uint32_t &bad) {
     bad = 1u;
     return 0.0f;
   }
-  return s;
+  return s == 0.0f ? 0.0f : s;  // -0 becomes +0 (the top-k keys are the score bits)
 }
 
 __device__ __forceinline__ float token_pi(bool tail, float s, float lam, float eps) {
@@ -82,6 +84,27 @@ __device__ __forceinline__ void block_minmax(float &mx, float &mn, BlockRed &R, 
   buf ^= 1;
 }
 
+// Inclusive prefix sum over the wave (64-bit).
+__device__ __forceinline__ uint64_t wave_scan_u64(uint64_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Systematic design: points s + k 2^32 (k >= 0) strictly below C.
+__device__ __forceinline__ uint64_t points_below(uint64_t C, uint32_t s) {
+  return C > (uint64_t)s ? ((C - (uint64_t)s - 1u) >> 32) + 1u : 0u;
+}
+
+// Integer weight of a stored pi: ceil(pi 2^32), the Poisson test's exact threshold.
+__device__ __forceinline__ uint64_t pi_weight(float pi) {
+  return (uint64_t)ceilf(pi * 4294967296.0f);
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
@@ -91,6 +114,9 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
   extern __shared__ float s_sc[];
   __shared__ BlockRed R;
   __shared__ int s_tot[2][kSelectThreads / 64];
+  __shared__ unsigned long long s_tot64[2][kSelectThreads / 64];
+  __shared__ int s_hist[256];
+  __shared__ int s_sel[2];
   int rbuf = 0;
   const int u = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -115,11 +141,13 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
   const int64_t ngroups = (n + 3) / 4;
   const int64_t tail_lo = L.n_sink, tail_hi = n - (int64_t)L.n_recent;  // T = [tail_lo, tail_hi)
   const bool staged = L.stage_rows > 0;
+  const bool uniform = L.design == EBD_DESIGN_UNIFORM;  // tail scores taken as 1, not read
   const bool vec = ((base & 3) == 0);  // 16-byte aligned score groups
 
   // Raw scores of group gi (0 past the end).
   auto load_raw = [&](int64_t gi) -> float4 {
     const int64_t i = 4 * gi;
+    if (uniform) return make_float4(1.0f, 1.0f, 1.0f, 1.0f);
     if (vec && i + 3 < n) return reinterpret_cast<const float4 *>(sc)[gi];
     float4 r;
     r.x = i < n ? sc[i] : 0.0f;
@@ -194,7 +222,67 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
 
   const double n_zero = n_tail - n_pos;
   double lam = 0.0;
-  if (n_tail == 0.0) {
+  const bool topk = L.design == EBD_DESIGN_TOPK;
+  // Top-k: k = floor(m + 1/2) tail positions; tkey is the k-th largest key (score bits, which
+  // order like the non-negative scores) and tleft how many positions equal to it to keep.
+  int64_t k_top = 0;
+  uint32_t tkey = 0xffffffffu;
+  int tleft = 0;
+  if (topk) {
+    k_top = (int64_t)floor(m + 0.5);
+    if (k_top < 0) k_top = 0;
+    if (k_top >= (int64_t)n_tail) {
+      k_top = (int64_t)n_tail;
+      if (n_tail > 0.0) st |= EBD_ST_NO_EVICTION;
+    }
+    if (k_top > 0 && k_top < (int64_t)n_tail) {
+      // radix select over the cleaned tail scores, 8 bits per pass from the top
+      uint32_t prefix = 0, pmask = 0;
+      int krem = (int)k_top;
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        s_hist[t] = 0;  // kSelectThreads == 256 bins
+        __syncthreads();
+        for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
+          const float4 s4 = group(gi);
+          const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t key = __float_as_uint(sv[j]);
+            if (sv[j] >= 0.0f && (key & pmask) == prefix)
+              atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+          }
+        }
+        __syncthreads();
+        // counts from the top digit down: thread t holds digit 255 - t
+        const int hv = s_hist[255 - t];
+        int incl = hv;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o);
+          if (lane >= o) incl += y;
+        }
+        if (lane == 63) s_tot[rbuf][wv] = incl;
+        __syncthreads();
+        for (int w = 0; w < wv; ++w) incl += s_tot[rbuf][w];
+        rbuf ^= 1;
+        if (incl >= krem && incl - hv < krem) {  // the digit holding the krem-th largest key
+          s_sel[0] = 255 - t;
+          s_sel[1] = krem - (incl - hv);
+        }
+        __syncthreads();
+        prefix |= (uint32_t)s_sel[0] << shift;
+        pmask |= 255u << shift;
+        krem = s_sel[1];
+        __syncthreads();
+      }
+      tkey = prefix;
+      tleft = krem;
+    } else if (k_top == (int64_t)n_tail) {
+      tkey = 0u;  // every tail key (+0.0 and up) is at or above it: keep all
+      tleft = INT32_MAX;
+    }
+  }
+  if (topk || n_tail == 0.0) {
     lam = 0.0;
   } else if (L.pi_mode == 1) {
     lam = (s_sum > 0.0 && m > 0.0) ? m / s_sum : 0.0;
@@ -256,26 +344,108 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
   // from per-wave ballots plus the counts of the lower waves.
   const uint64_t sd = L.seed_per_unit ? L.seed_per_unit[u] : L.seed;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int design = L.design;
+  // systematic design: one start per unit and the cumulative integer weight so far
+  const uint32_t sys_start =
+      philox4x32_10(make_uint4(0u, (uint32_t)u, L.epoch, kSystematicTag), (uint32_t)sd,
+                    (uint32_t)(sd >> 32)).x;
+  uint64_t csum = 0;
+  int64_t eq_seen = 0;  // top-k: tail positions equal to the threshold key so far
   int64_t rank0 = 0;
   for (int64_t g0 = 0; g0 < ngroups; g0 += kSelectThreads) {
     const int64_t gi = g0 + t;
     float p[4] = {1.0f, 1.0f, 1.0f, 1.0f};
     bool keep[4] = {false, false, false, false};
+    bool inr[4] = {false, false, false, false};
+    float sv[4] = {-1.0f, -1.0f, -1.0f, -1.0f};
     if (gi < ngroups) {
       const float4 s4 = group(gi);
-      const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
-      const uint4 x = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)u, L.epoch, kPhiloxTag),
-                                    (uint32_t)sd, (uint32_t)(sd >> 32));
-      const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+      sv[0] = s4.x;
+      sv[1] = s4.y;
+      sv[2] = s4.z;
+      sv[3] = s4.w;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int64_t i = 4 * gi + j;
-        if (i < n) {
-          p[j] = token_pi(sv[j] >= 0.0f, sv[j], lamf, eps);
-          keep[j] = keep_token(xw[j], p[j]);
-          if (L.pi_full) L.pi_full[base + i] = p[j];
-        }
+        inr[j] = 4 * gi + j < n;
+        if (inr[j] && !topk) p[j] = token_pi(sv[j] >= 0.0f, sv[j], lamf, eps);
       }
+    }
+    if (design == EBD_DESIGN_SYSTEMATIC) {
+      uint64_t a[4], tsum = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a[j] = inr[j] ? pi_weight(p[j]) : 0u;
+        tsum += a[j];
+      }
+      const uint64_t incl = wave_scan_u64(tsum);
+      if (lane == 63) s_tot64[rbuf][wv] = incl;
+      __syncthreads();
+      uint64_t wpre = 0, btot = 0;
+#pragma unroll
+      for (int w = 0; w < kSelectThreads / 64; ++w) {
+        const uint64_t c = s_tot64[rbuf][w];
+        wpre += w < wv ? c : 0u;
+        btot += c;
+      }
+      uint64_t C = csum + wpre + incl - tsum;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint64_t Cn = C + a[j];
+        keep[j] = inr[j] && points_below(Cn, sys_start) != points_below(C, sys_start);
+        C = Cn;
+      }
+      csum += btot;
+    } else if (topk) {
+      // tail positions at the threshold key are kept in position order while tleft lasts
+      bool eq[4];
+      int ebefore = 0, etot = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        eq[j] = inr[j] && sv[j] >= 0.0f && __float_as_uint(sv[j]) == tkey;
+        const uint64_t bal = __ballot(eq[j]);
+        ebefore += __popcll(bal & below);
+        etot += __popcll(bal);
+      }
+      if (lane == 0) s_tot[rbuf][wv] = etot;
+      __syncthreads();
+      int ewpre = 0, ebtot = 0;
+#pragma unroll
+      for (int w = 0; w < kSelectThreads / 64; ++w) {
+        const int c = s_tot[rbuf][w];
+        ewpre += w < wv ? c : 0;
+        ebtot += c;
+      }
+      rbuf ^= 1;
+      // rank of this thread's first equal position among the unit's equal positions: the
+      // earlier blocks, the lower waves, then the lower lanes of this wave (positions ascend
+      // with block, wave and lane; within a thread, with j)
+      int64_t er = eq_seen + ewpre + ebefore;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool tail = sv[j] >= 0.0f;
+        bool sel = false;
+        if (inr[j] && tail) {
+          const uint32_t key = __float_as_uint(sv[j]);
+          if (key > tkey) sel = true;
+          else if (eq[j]) sel = er++ < (int64_t)tleft;
+        }
+        p[j] = (!inr[j] || !tail) ? 1.0f : (sel ? 1.0f : 0.0f);
+        keep[j] = inr[j] && (!tail || sel);
+      }
+      eq_seen += ebtot;
+    } else {
+      if (gi < ngroups) {
+        const uint4 x = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)u, L.epoch, kPhiloxTag),
+                                      (uint32_t)sd, (uint32_t)(sd >> 32));
+        const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) keep[j] = inr[j] && keep_token(xw[j], p[j]);
+      }
+    }
+    if (L.pi_full) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (inr[j]) L.pi_full[base + 4 * gi + j] = p[j];
     }
     int before = 0, wtot = 0;
 #pragma unroll

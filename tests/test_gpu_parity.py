@@ -60,7 +60,7 @@ def _evict(K, V, seq_off, sc, lengths, **kw):
 
 
 def _check_evict(lengths, K, V, seq_off, sc, out, n_sink=4, n_recent=64, budget=0.1, pi_min=0.01,
-                 seed=0, pi_mode=0, epoch=0):
+                 seed=0, pi_mode=0, epoch=0, design=0):
     Kb, Vb = _bits(K), _bits(V)
     off = _np(seq_off)
     coff = _np(out.cap_off)
@@ -68,14 +68,14 @@ def _check_evict(lengths, K, V, seq_off, sc, out, n_sink=4, n_recent=64, budget=
     pi_gpu = _np(out.pi_full)[: off[-1]]
     # (1) pi against the oracle's fp64 solve
     ref = oracle.evict_batch(off, coff, s, Kb, Vb, n_sink, n_recent, budget_frac=budget,
-                             pi_min=pi_min, seed=seed, epoch=epoch, pi_mode=pi_mode)
+                             pi_min=pi_min, seed=seed, epoch=epoch, pi_mode=pi_mode, design=design)
     assert np.max(np.abs(pi_gpu - ref["pi_full"]), initial=0.0) <= 1e-5
     st_gpu = _np(out.status).astype(np.uint32) & ~np.uint32(oracle.ST_CAP_OVERFLOW)
     st_ref = ref["status"] & ~np.uint32(oracle.ST_CAP_OVERFLOW)
     np.testing.assert_array_equal(st_gpu, st_ref)
     # (2) mask and compaction bit-exact given the GPU's pi
     same = oracle.evict_batch(off, coff, s, Kb, Vb, n_sink, n_recent, pi_given=pi_gpu, seed=seed,
-                              epoch=epoch)
+                              epoch=epoch, design=design)
     cnt = _np(out.count)
     np.testing.assert_array_equal(cnt, same["count"])
     np.testing.assert_array_equal(_np(out.status).astype(np.uint32) & oracle.ST_CAP_OVERFLOW,
@@ -187,6 +187,70 @@ def test_evict_deterministic():
     c = _evict(K, V, seq_off, sc, lengths, budget_frac=0.25, seed=5, epoch=1)
     k = int(min(a.count[0], c.count[0]))
     assert not torch.equal(a.idxc[:k], c.idxc[:k])
+
+
+# ------------------------------------------------------------------------------------------
+# Other designs: fixed-size systematic, top-k and uniform comparison arms
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("lengths,budget", [
+    ([4096] * 8, 0.10),
+    ([0, 1, 5, 70, 100, 777, 2047, 2048, 2049, 5000, 16384], 0.25),
+    ([20000, 40001, 3], 0.1),                 # streamed scores
+])
+def test_evict_systematic_design(lengths, budget):
+    _say("evict systematic lengths=%s budget=%s" % (lengths[:6], budget))
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=21)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=budget, seed=12,
+                 design=oracle.DESIGN_SYSTEMATIC)
+    cnt = _check_evict(lengths, K, V, seq_off, sc, out, budget=budget, seed=12,
+                       design=oracle.DESIGN_SYSTEMATIC)
+    # the size is fixed: floor or ceil of the unit's total integer weight / 2^32
+    off = _np(seq_off)
+    pi = _np(out.pi_full)
+    for u in range(len(lengths)):
+        a = np.ceil(pi[off[u]:off[u + 1]].astype(np.float64) * 2.0 ** 32).sum() / 2.0 ** 32
+        assert int(np.floor(a)) <= cnt[u] <= int(np.ceil(a))
+
+
+@pytest.mark.parametrize("lengths,budget,ties", [
+    ([4096] * 8, 0.10, False),
+    ([0, 1, 5, 70, 777, 2048, 5000, 16384], 0.3, True),   # integer scores: many ties
+    ([20000, 40001, 3], 0.1, True),                       # streamed scores
+    ([3000, 3000], 1.0, False),                           # k = |T|: keep everything
+])
+def test_evict_topk_design(lengths, budget, ties):
+    _say("evict top-k lengths=%s budget=%s ties=%s" % (lengths[:6], budget, ties))
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=22)
+    if ties:
+        sc = torch.floor(sc * 2000.0)
+        rows = sc.shape[0]
+        if rows > 40:
+            sc[7] = float("nan")
+            sc[30] = -0.0
+            sc[31] = -3.0
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=budget, seed=1, design=oracle.DESIGN_TOPK)
+    off, coff = _np(seq_off), _np(out.cap_off)
+    ref = oracle.evict_batch(off, coff, _np(sc), _bits(K), _bits(V), 4, 64, budget_frac=budget,
+                             design=oracle.DESIGN_TOPK)
+    np.testing.assert_array_equal(_np(out.pi_full)[: off[-1]], ref["pi_full"])
+    np.testing.assert_array_equal(_np(out.count), ref["count"])
+    np.testing.assert_array_equal(_np(out.status).astype(np.uint32), ref["status"])
+    for u in range(len(lengths)):
+        a, k = coff[u], int(ref["count"][u])
+        np.testing.assert_array_equal(_np(out.idxc)[a:a + k], ref["idx"][a:a + k])
+        np.testing.assert_array_equal(_bits(out.Kc)[a:a + k], ref["Kc"][a:a + k])
+        np.testing.assert_array_equal(_bits(out.Vc)[a:a + k], ref["Vc"][a:a + k])
+
+
+def test_evict_uniform_design():
+    lengths = [4096, 333, 6144, 20000]
+    _say("evict uniform")
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=23)
+    sc = sc.clone()
+    sc[5] = float("nan")  # not read by the uniform design: no flag
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.2, seed=4, design=oracle.DESIGN_UNIFORM)
+    _check_evict(lengths, K, V, seq_off, sc, out, budget=0.2, seed=4, design=oracle.DESIGN_UNIFORM)
+    assert not (_np(out.status) & oracle.ST_BAD_SCORE).any()
 
 
 # ------------------------------------------------------------------------------------------
