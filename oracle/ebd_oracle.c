@@ -364,7 +364,10 @@ int64_t ebd_ref_compact(int64_t n, int32_t d, const uint8_t *mask, const float *
  *   q [G, d] bf16 bits; Kc, Vc [count, d] bf16 bits; pic [count] stored pi.
  *   a_j = exp(s_j - M) with s_j = scale q.k_j and M = max_j s_j (the common
  *   factor exp(-M) cancels in yhat, Vhat, b and r; it is added back in lse).
- *   use_offset = 0 drops the 1/pi weights (uncorrected retained softmax).
+ *   use_offset = 0: y and lse are those of the uncorrected retained softmax (weights a_j,
+ *   no 1/pi), while Vhat, b and r stay the Hajek certificate of the same retained set
+ *   (App. "Experimental details": runs with the uncorrected softmax computed the
+ *   certificate as the Hajek radius).
  * Outputs per head: y [G, d], vhat, lse = ln Nhat, brange, radius.
  */
 void ebd_ref_attend_certify(int32_t G, int32_t d, int64_t count, const uint16_t *q,
@@ -375,14 +378,16 @@ void ebd_ref_attend_certify(int32_t G, int32_t d, int64_t count, const uint16_t 
     double *s = (double *)malloc((size_t)(count > 0 ? count : 1) * sizeof(double));
     double *a = (double *)malloc((size_t)(count > 0 ? count : 1) * sizeof(double));
     double *qd = (double *)malloc((size_t)d * sizeof(double));
+    double *yhaj = (double *)malloc((size_t)d * sizeof(double));
     const double log_inv_delta = log(1.0 / delta);
 
     for (int32_t h = 0; h < G; ++h) {
-        double *yh = y + (int64_t)h * d;
+        double *yh = yhaj; /* the Hajek output, for the certificate */
         for (int32_t c = 0; c < d; ++c) {
             qd[c] = ref_bf16(q[(int64_t)h * d + c]);
             yh[c] = 0.0;
         }
+        for (int32_t c = 0; c < d; ++c) y[(int64_t)h * d + c] = 0.0;
         if (count == 0) {
             vhat[h] = 0.0;
             lse[h] = -INFINITY;
@@ -402,13 +407,11 @@ void ebd_ref_attend_certify(int32_t G, int32_t d, int64_t count, const uint16_t 
         double Nhat = 0.0;
         for (int64_t j = 0; j < count; ++j) {
             a[j] = exp(s[j] - M);
-            double pj = use_offset ? (double)pic[j] : 1.0;
-            Nhat += a[j] / pj;
+            Nhat += a[j] / (double)pic[j];
         }
         /* yhat = sum_S (a_j / pi_j) v_j / Nhat (eq. (3)) */
         for (int64_t j = 0; j < count; ++j) {
-            double pj = use_offset ? (double)pic[j] : 1.0;
-            double wj = a[j] / pj / Nhat;
+            double wj = a[j] / (double)pic[j] / Nhat;
             for (int32_t c = 0; c < d; ++c) yh[c] += wj * ref_bf16(Vc[j * d + c]);
         }
         /* Theorem 2 and eq. (4): sums over S cap T (pi < 1; pi = 1 terms vanish) */
@@ -429,13 +432,27 @@ void ebd_ref_attend_certify(int32_t G, int32_t d, int64_t count, const uint16_t 
         for (int32_t c = 0; c < d; ++c) ynorm += yh[c] * yh[c];
         ynorm = sqrt(ynorm);
         vhat[h] = V;
-        lse[h] = M + log(Nhat);
         if (brange) brange[h] = bmax;
         if (radius) radius[h] = (sqrt(2.0 * V * log_inv_delta) + bmax * log_inv_delta) / (ynorm + eps0);
+        double *yo = y + (int64_t)h * d;
+        if (use_offset) {
+            for (int32_t c = 0; c < d; ++c) yo[c] = yh[c];
+            lse[h] = M + log(Nhat);
+        } else {
+            /* uncorrected retained softmax: weights a_j, normaliser sum_S a_j */
+            double N0 = 0.0;
+            for (int64_t j = 0; j < count; ++j) N0 += a[j];
+            for (int64_t j = 0; j < count; ++j) {
+                double wj = a[j] / N0;
+                for (int32_t c = 0; c < d; ++c) yo[c] += wj * ref_bf16(Vc[j * d + c]);
+            }
+            lse[h] = M + log(N0);
+        }
     }
     free(s);
     free(a);
     free(qd);
+    free(yhaj);
 }
 
 /* Full-cache head output, eq. (1): y = sum_C a_i v_i / sum_C a_i, for G heads. */

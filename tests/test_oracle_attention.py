@@ -71,9 +71,13 @@ def test_logit_offset_equals_ratio_form():
     np.testing.assert_allclose(out["y"], _sdpa(q, K, V, bias=bias), rtol=1e-12, atol=1e-13)
     s = bf16_to_f64(q) @ bf16_to_f64(K).T / np.sqrt(d) + bias[None, :]
     np.testing.assert_allclose(out["lse"], torch.logsumexp(torch.tensor(s), 1).numpy(), rtol=1e-13)
-    # use_offset = False is the uncorrected retained softmax
+    # use_offset = False: the uncorrected retained softmax as output, the Hajek certificate
     out0 = oracle.attend_certify(q, K, V, pi, use_offset=False)
     np.testing.assert_allclose(out0["y"], _sdpa(q, K, V), rtol=1e-12, atol=1e-13)
+    s0 = bf16_to_f64(q) @ bf16_to_f64(K).T / np.sqrt(d)
+    np.testing.assert_allclose(out0["lse"], torch.logsumexp(torch.tensor(s0), 1).numpy(), rtol=1e-13)
+    for key in ("vhat", "b", "r"):
+        np.testing.assert_array_equal(out0[key], out[key])
 
 
 def _case(seed, G=2, n=200, d=128, loc=0.0):
