@@ -139,8 +139,13 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
  *   (0 means 1e-9): the confidence level and normaliser of eq. (4).
  *   split_rows: retained rows per split, one wave each (0 = library choice; else a
  *   multiple of 16 in [16, 8192]).  Retained rows of a unit beyond max_rows are ignored.
- *   flags: reserved, must be 0.
+ *   flags: 0, or EBD_F_NO_OFFSET: y and ln N are those of the uncorrected retained softmax
+ *   (the logit offset -ln pi dropped, the ablation arm of Sec. 5 and App. "Experimental
+ *   details"), while vhat, b and r stay the Hajek certificate of the same retained set;
+ *   costs a second pass over the retained rows.
  */
+#define EBD_F_NO_OFFSET 1u
+
 typedef struct ebd_attend_params {
     int32_t num_units;
     int32_t group;

@@ -44,6 +44,8 @@ EBD_DESIGN_SYSTEMATIC = 1
 EBD_DESIGN_TOPK = 2
 EBD_DESIGN_UNIFORM = 3
 
+EBD_F_NO_OFFSET = 1
+
 EBD_WS_EVICT = 0
 EBD_WS_ATTEND = 1
 EBD_WS_SCORES = 2
@@ -188,7 +190,7 @@ def evict_params(num_units, max_rows, max_capacity, seq_off, cap_off, n_sink=4, 
 
 
 def attend_params(num_units, group, max_rows, cap_off, split_rows=0, scale=0.0, delta=0.1,
-                  eps0=1e-9) -> ebd_attend_params:
+                  eps0=1e-9, flags=0) -> ebd_attend_params:
     p = ebd_attend_params()
     p.num_units = int(num_units)
     p.group = int(group)
@@ -199,7 +201,7 @@ def attend_params(num_units, group, max_rows, cap_off, split_rows=0, scale=0.0, 
     p.scale = float(scale)
     p.delta = float(delta)
     p.eps0 = float(eps0)
-    p.flags = 0
+    p.flags = int(flags)
     return p
 
 

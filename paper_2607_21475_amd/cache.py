@@ -11,7 +11,7 @@ from typing import Optional, Sequence, Union
 
 import torch
 
-from . import (EBD_WS_ATTEND, EBD_WS_EVICT, EBD_WS_SCORES, HEAD_DIM, attend_params,
+from . import (EBD_F_NO_OFFSET, EBD_WS_ATTEND, EBD_WS_EVICT, EBD_WS_SCORES, HEAD_DIM, attend_params,
                ebd_attend_certify, ebd_evict, ebd_scores, ebd_workspace_size, evict_params,
                scores_params, workspace)
 
@@ -100,11 +100,13 @@ def evict(K: torch.Tensor, V: torch.Tensor, scores: torch.Tensor, seq_off: torch
 
 
 def attend_certify(cache: RetainedCache, q: torch.Tensor, split_rows: int = 0, delta: float = 0.1,
-                   eps0: float = 1e-9, scale: float = 0.0, ws: Optional[torch.Tensor] = None):
+                   eps0: float = 1e-9, scale: float = 0.0, ws: Optional[torch.Tensor] = None,
+                   offset: bool = True):
     """Outputs y [U, G, 128], vhat, lse, b, r [U, G] (fp32) and the workspace used."""
     U, G, _ = q.shape
     dev = q.device
-    p = attend_params(U, G, cache.max_cap, cache.cap_off, split_rows, scale, delta, eps0)
+    p = attend_params(U, G, cache.max_cap, cache.cap_off, split_rows, scale, delta, eps0,
+                      0 if offset else EBD_F_NO_OFFSET)
     need = ebd_workspace_size(EBD_WS_ATTEND, p)
     if ws is None or ws.numel() < need:
         ws = workspace(need, dev)

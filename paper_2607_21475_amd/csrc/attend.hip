@@ -84,7 +84,7 @@ constexpr float kLazy = 8.0f;
 // lane's row group are real (<= 0 masks them all), `rowbase` is the unit row of its first one.
 __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const bf16x8 (&qop)[4],
                                            int nvalid, int rowbase, bool isC, bool mine,
-                                           float scale2) {
+                                           bool plain, float scale2) {
   f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
@@ -93,7 +93,7 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
   // log2 pi of the 4 rows of this row group: quad lane i computes row i, the quad shares it.
   const int qi = __lane_id() & 3;
   const float pq = qi == 0 ? T.p[0] : (qi == 1 ? T.p[1] : (qi == 2 ? T.p[2] : T.p[3]));
-  const float lq = fast_log2(pq);
+  const float lq = plain ? 0.0f : fast_log2(pq);  // the uncorrected pass drops the offset
   float lp[4];
   lp[0] = dpp_f<0x00>(lq);  // quad_perm [0,0,0,0]
   lp[1] = dpp_f<0x55>(lq);  // quad_perm [1,1,1,1]
@@ -317,7 +317,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       float *hs = F.hs + h * kHs;
       const float l = hs[kHsL];
       const float V = fmaxf(hs[kHsC2] - 2.0f * ycv + yy * hs[kHsC0], 0.0f) / (l * l);
-      L.vhat[uh0 + h] = V;
+      if (!L.plain) L.vhat[uh0 + h] = V;
       L.lse[uh0 + h] = hs[kHsM] * kLn2 + logf(l);
       hs[kHsYn] = sqrtf(yy);
       hs[kHsLb] = 0.0f;
@@ -326,6 +326,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     }
   }
   __syncthreads();
+  if (L.plain) return;  // the uncorrected pass only replaces y and ln N
 
   // (2) Candidate bounds: a candidate's value f g |v - yhat| / l is at most f g (Vmax + |yhat|)/l.
   //     Candidate e = ((s nchunk + k) GB + h) kCand + j.
@@ -546,12 +547,14 @@ __device__ void finalize_empty(const AttendLaunch &L, int u, int h0) {
   const int64_t uh0 = (int64_t)u * L.G + h0;
   for (int e = lane; e < GB * kHeadDim; e += 64) L.y[uh0 * kHeadDim + e] = 0.0f;
   if (lane < GB) {
-    L.vhat[uh0 + lane] = 0.0f;
     L.lse[uh0 + lane] = -INFINITY;
-    if (L.brange) L.brange[uh0 + lane] = 0.0f;
-    if (L.radius) L.radius[uh0 + lane] = 0.0f;
+    if (!L.plain) {
+      L.vhat[uh0 + lane] = 0.0f;
+      if (L.brange) L.brange[uh0 + lane] = 0.0f;
+      if (L.radius) L.radius[uh0 + lane] = 0.0f;
+    }
   }
-  if (lane == 0) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+  if (lane == 0 && !L.plain) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
 }
 
 // One wave per (unit, split, head block).  Lane (g, c): MFMA column c is head slot c (weights for
@@ -608,6 +611,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   const __amdgpu_buffer_rsrc_t rV = make_rsrc(L.Vc + r0 * kHeadDim, (uint32_t)nrow * 256u);
   const __amdgpu_buffer_rsrc_t rP = make_rsrc(L.pic + r0, (uint32_t)nrow * 4u);
   const float scale2 = L.scale * kLog2e;
+  const bool plain = L.plain != 0;
   const int ntile = (nrow + 15) / 16;
   const int nv0 = active ? nrow - 4 * g : -1;  // valid rows of this lane's row group in tile 0
   const int rb0 = row0 + 4 * g;
@@ -620,7 +624,8 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   constexpr int kChunkTiles = kChunkRows / 16;
   // tile tt of the split, then the flush of its chunk if tt ends one
   auto step = [&](const Tile &T, int tt) {
-    split_tile(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, isC == ((tt & 1) != 0), scale2);
+    split_tile(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, isC == ((tt & 1) != 0), plain,
+               scale2);
     if ((tt + 1) % kChunkTiles == 0)
       flush_chunk<GB>(S, s_chunk, tt / kChunkTiles, g, c, row0 + (tt / kChunkTiles) * kChunkRows);
   };
@@ -666,7 +671,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
       F.hs[(c - GB) * kHs + kHsC0] = s0;
       F.hs[(c - GB) * kHs + kHsC2] = s1;
     }
-    if (lane == 0) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+    if (lane == 0 && !L.plain) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
     __syncthreads();
     const CandSrc C{s_chunk, 0, GB * kChunkFloats, kChunkFloats};
     finalize_block<GB>(L, u, h0, cnt, cbase, 1, C, F);
@@ -718,7 +723,7 @@ __global__ __launch_bounds__(64) void attend_finalize_kernel(AttendLaunch L, int
     finalize_empty<GB>(L, u, h0);
     return;
   }
-  if (lane == 0) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+  if (lane == 0 && !L.plain) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
   const int nsp = (cnt + L.split_rows - 1) / L.split_rows;
   const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h0) * L.rec;  // (s, h) at s G rec + h rec
   const int64_t sstride = (int64_t)L.G * L.rec;

@@ -151,7 +151,7 @@ bool valid_attend_params(const ebd_attend_params *p) {
   if (p->split_rows != 0 &&
       (p->split_rows < 16 || p->split_rows > kSplitRowsLimit || p->split_rows % 16))
     return false;
-  if (p->flags != 0u) return false;
+  if ((p->flags & ~EBD_F_NO_OFFSET) != 0u) return false;
   if (p->scale < 0.0f || !std::isfinite(p->scale)) return false;
   if (p->delta < 0.0f || p->delta >= 1.0f) return false;
   if (p->eps0 < 0.0f || !std::isfinite(p->eps0)) return false;
@@ -294,11 +294,16 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
   L.radius = radius;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (timed("attend_split", s, [&] { return launch_attend_split(L, s); }) != hipSuccess)
-    return EBD_ERR_HIP;
-  if (L.nsplit > 1 &&
-      timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
-    return EBD_ERR_HIP;
+  L.plain = 0;
+  const int passes = (p->flags & EBD_F_NO_OFFSET) ? 2 : 1;
+  for (int pass = 0; pass < passes; ++pass) {
+    L.plain = pass;  // the second pass replaces y and ln N by the uncorrected softmax
+    if (timed("attend_split", s, [&] { return launch_attend_split(L, s); }) != hipSuccess)
+      return EBD_ERR_HIP;
+    if (L.nsplit > 1 &&
+        timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
+      return EBD_ERR_HIP;
+  }
   return EBD_OK;
 }
 

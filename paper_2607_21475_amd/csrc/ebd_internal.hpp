@@ -75,6 +75,7 @@ struct EvictLaunch {
 struct AttendLaunch {
   int32_t U, G, nsplit, split_rows, nhb;
   int32_t nchunk, rec;  // chunks per split, floats per record
+  int32_t plain;        // 1: the uncorrected pass (no offset; writes y and lse only)
   const int64_t *cap_off;
   const int32_t *count;
   const uint16_t *q, *Kc, *Vc;

@@ -116,7 +116,7 @@ def test_attend_argument_validation():
     assert call(params(d=96)) == ebd.EBD_ERR_UNSUPPORTED
     assert call(params(G=0)) == ebd.EBD_ERR_INVALID_ARG
     assert call(params(split=100)) == ebd.EBD_ERR_INVALID_ARG
-    assert call(params(flags=1)) == ebd.EBD_ERR_INVALID_ARG
+    assert call(params(flags=2)) == ebd.EBD_ERR_INVALID_ARG  # only EBD_F_NO_OFFSET is defined
     assert call(params(delta=1.0)) == ebd.EBD_ERR_INVALID_ARG
     assert call(params(), ws_bytes=100) == ebd.EBD_ERR_WORKSPACE
     assert call(params(U=0)) == ebd.EBD_OK

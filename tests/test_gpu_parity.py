@@ -299,6 +299,36 @@ def test_attend_parity(lengths, G, budget, split):
     _check_attend(out, res, q, G)
 
 
+@pytest.mark.parametrize("lengths,G,split", [
+    ([6144] * 6, 7, 0),                       # fused finalize
+    ([4096, 300, 0, 9000], 4, 256),           # several splits, an empty unit
+])
+def test_attend_without_offset(lengths, G, split):
+    """EBD_F_NO_OFFSET: the uncorrected retained softmax as output, the Hajek certificate."""
+    _say("attend no-offset lengths=%s G=%d split=%d" % (lengths, G, split))
+    from paper_2607_21475_amd import cache
+
+    K, V, seq_off, sc, q = _inputs(lengths, seed=31, group=G)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.25, seed=3)
+    res = cache.attend_certify(out, q, split_rows=split, offset=False)
+    ref_h = cache.attend_certify(out, q, split_rows=split)
+    torch.cuda.synchronize()
+    coff, cnt = _np(out.cap_off), _np(out.count)
+    ref = oracle.attend_batch(coff, cnt, _bits(q), _bits(out.Kc), _bits(out.Vc), _np(out.pic),
+                              use_offset=False)
+    y = _np(res["y"]).astype(np.float64)
+    nrm = np.linalg.norm(ref["y"], axis=2)
+    live = cnt > 0
+    assert np.all(np.linalg.norm(y - ref["y"], axis=2)[live] <= 2e-3 * nrm[live])
+    lse = _np(res["lse"]).astype(np.float64)
+    assert np.all(np.abs(lse[live] - ref["lse"][live]) <= 1e-4 * np.maximum(1.0, np.abs(ref["lse"][live])))
+    for key in ("vhat", "b", "r"):  # the certificate does not depend on the flag
+        np.testing.assert_array_equal(_np(res[key]), _np(ref_h[key]))
+        g = _np(res[key]).astype(np.float64)
+        floor = 1e-6 * nrm ** (2 if key == "vhat" else 1) + 1e-30
+        assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.maximum(np.abs(ref[key]), floor)), key
+
+
 def test_attend_empty_and_tiny_units():
     _say("attend empty units")
     from paper_2607_21475_amd import cache
