@@ -90,6 +90,10 @@ def _load():
     lib.ebd_ref_window_scores.restype = None
     lib.ebd_ref_window_scores_batch.argtypes = [i32, i32, i32, P, P, P, P, f64, P, i32]
     lib.ebd_ref_window_scores_batch.restype = None
+    lib.ebd_ref_block_contributions.argtypes = [i32, i32, i64, P, P, P, P, P, P, P, f64, i32, i64, P]
+    lib.ebd_ref_block_contributions.restype = None
+    lib.ebd_ref_certificate_step.argtypes = [i32, i32, i32, i32, P, P, P, P, P]
+    lib.ebd_ref_certificate_step.restype = None
     lib.ebd_ref_max_threads.argtypes = []
     lib.ebd_ref_max_threads.restype = i32
     _lib = lib
@@ -336,3 +340,43 @@ def window_scores_batch(seq_off, K, Q, qpos=None, scale=None, nthreads=0):
     _load().ebd_ref_window_scores_batch(U, d, W, _p(off), _p(K), _p(Q), _p(qp), float(scale),
                                         _p(out), int(nthreads))
     return out
+
+
+# --------------------------------------------------------------------------
+# Fine-grained attribution and the deployed certificate (Sec. 6; App. details)
+# --------------------------------------------------------------------------
+def block_contributions(q, Kc, Vc, pic, idx, yhat, lse, nblocks, block_rows=64, scale=None):
+    """Sum over heads and over retained tokens in each block of original positions of the
+    Theorem 2 summand (1-pi)/pi^2 a^2 |v - yhat|^2 / Nhat^2.  q [G, d]; yhat [G, d]; lse [G]."""
+    q = _c(q, np.uint16)
+    if q.ndim == 1:
+        q = q[None, :]
+    G, d = q.shape
+    Kc = _c(Kc, np.uint16).reshape(-1, d)
+    Vc = _c(Vc, np.uint16).reshape(-1, d)
+    count = Kc.shape[0]
+    pic = _c(pic, np.float32)
+    idx = _c(idx, np.int32)
+    yh = _c(yhat, np.float64).reshape(G, d)
+    ls = _c(lse, np.float64).reshape(G)
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.zeros(max(int(nblocks), 1), np.float64)
+    _load().ebd_ref_block_contributions(G, d, count, _p(q), _p(Kc), _p(Vc), _p(pic), _p(idx),
+                                        _p(yh), _p(ls), float(scale), int(block_rows),
+                                        int(nblocks), _p(out))
+    return out[: int(nblocks)]
+
+
+def certificate_step(radius, unit_seq, num_seqs, head_stride=4, unit_head0=None, cert=None):
+    """Mean radius over the sampled (unit, head) pairs per sequence, folded into the running
+    maximum `cert` (returned with the means)."""
+    r = _c(radius, np.float32)
+    U, G = r.shape
+    us = _c(unit_seq, np.int32)
+    h0 = None if unit_head0 is None else _c(unit_head0, np.int32)
+    c = np.zeros(num_seqs, np.float64) if cert is None else _c(cert, np.float64).copy()
+    mean = np.zeros(num_seqs, np.float64)
+    _load().ebd_ref_certificate_step(U, G, num_seqs, head_stride, _p(us), _p(h0), _p(r), _p(c),
+                                     _p(mean))
+    return c, mean

@@ -15,6 +15,9 @@
  *     Sec. 3.3  Theorem 2  Vhat = Nhat^-2 sum_{S cap T} (1-pi)/pi^2 a^2 |v - yhat|^2
  *     Sec. 3.4  eq. (4)  radius r = (sqrt(2 Vhat ln(1/delta)) + b ln(1/delta)) / (|yhat| + eps0)
  *                        b = max_{S cap T} sqrt((1-pi)/pi^2) a |v - yhat| / Nhat
+ *   Sec. 6 "Finer grains" and the fine-grained probe: per-token variance contributions
+ *     pooled into blocks of original positions; the deployed certificate (mean radius
+ *     over sampled heads, maximum over decode steps)
  *   App. "Experimental details", Harness: importance scores from accumulated attention
  *     (strided prefill queries) or an observation window of queries: per query, the
  *     softmax over the keys it sees, summed over the queries
@@ -484,6 +487,71 @@ void ebd_ref_full_attention(int32_t G, int32_t d, int64_t n, const uint16_t *q, 
     }
     free(s);
     free(qd);
+}
+
+/* ------------------------------------------------------------------ */
+/* Fine-grained attribution (Sec. 6 "Finer grains"; App. "Experimental */
+/* details", fine-grained probe): the variance contribution of each    */
+/* retained token, kappa_hj = (1-pi_j)/pi_j^2 a_hj^2 |v_j - yhat_h|^2 / */
+/* Nhat_h^2 (the summand of Theorem 2), summed over the unit's query   */
+/* heads and over the retained tokens whose original position lies in  */
+/* each block of `block_rows` positions.  yhat and ln Nhat are inputs  */
+/* (the outputs of the certified attention).                           */
+/* ------------------------------------------------------------------ */
+void ebd_ref_block_contributions(int32_t G, int32_t d, int64_t count, const uint16_t *q,
+                                 const uint16_t *Kc, const uint16_t *Vc, const float *pic,
+                                 const int32_t *idx, const double *yhat, const double *lse,
+                                 double scale, int32_t block_rows, int64_t nblocks, double *out)
+{
+    double *qd = (double *)malloc((size_t)d * sizeof(double));
+    for (int64_t b = 0; b < nblocks; ++b) out[b] = 0.0;
+    for (int32_t h = 0; h < G; ++h) {
+        for (int32_t c = 0; c < d; ++c) qd[c] = ref_bf16(q[(int64_t)h * d + c]);
+        const double *yh = yhat + (int64_t)h * d;
+        for (int64_t j = 0; j < count; ++j) {
+            if (idx[j] < 0) continue;  /* appended without a position (pi = 1: no term) */
+            const int64_t b = (int64_t)idx[j] / block_rows;
+            if (b >= nblocks) continue;
+            const double pj = (double)pic[j];
+            if (!(pj < 1.0)) continue;
+            double dot = 0.0, dist2 = 0.0;
+            for (int32_t c = 0; c < d; ++c) {
+                dot += qd[c] * ref_bf16(Kc[j * d + c]);
+                const double e = ref_bf16(Vc[j * d + c]) - yh[c];
+                dist2 += e * e;
+            }
+            /* a/(pi Nhat) = exp(scale q.k - ln pi - ln Nhat) */
+            const double wn = exp(scale * dot - log(pj) - lse[h]);
+            out[b] += (1.0 - pj) * wn * wn * dist2;
+        }
+    }
+    free(qd);
+}
+
+/* Deployed certificate (App. "Experimental details"): per sequence, the mean radius over the  */
+/* sampled (unit, query head) pairs -- query head index head0[u] + g a multiple of head_stride */
+/* -- folded into a running maximum over decode steps.  A sequence with no sampled pair keeps */
+/* its maximum; mean_out gets 0 for it.                                                      */
+void ebd_ref_certificate_step(int32_t U, int32_t G, int32_t S, int32_t head_stride,
+                              const int32_t *unit_seq, const int32_t *unit_head0,
+                              const float *radius, double *cert, double *mean_out)
+{
+    for (int32_t sq = 0; sq < S; ++sq) {
+        double sum = 0.0;
+        int64_t cnt = 0;
+        for (int32_t u = 0; u < U; ++u) {
+            if (unit_seq[u] != sq) continue;
+            for (int32_t g = 0; g < G; ++g) {
+                const int64_t hidx = (int64_t)(unit_head0 ? unit_head0[u] : 0) + g;
+                if (hidx % head_stride != 0) continue;
+                sum += (double)radius[(int64_t)u * G + g];
+                cnt++;
+            }
+        }
+        const double mean = cnt > 0 ? sum / (double)cnt : 0.0;
+        if (mean_out) mean_out[sq] = mean;
+        if (cnt > 0 && mean > cert[sq]) cert[sq] = mean;
+    }
 }
 
 /* ------------------------------------------------------------------ */
