@@ -158,7 +158,7 @@ def main() -> int:
     # Pre-plan every launch: outputs, workspaces and parameter blocks are allocated once.
     plans = []
     for b in budgets:
-        cap_host = cache.plan_capacity(lengths, b, wl.n_sink, wl.n_recent)
+        cap_host = cache.plan_capacity(lengths, b, wl.n_sink, wl.n_recent, pi_min=wl.pi_min)
         cap_off = torch.tensor(cap_host, dtype=torch.int64, device="cuda")
         rows = cap_host[-1]
         rc = cache.RetainedCache(

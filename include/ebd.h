@@ -230,6 +230,58 @@ typedef struct ebd_scores_params {
 ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint16_t *K,
                       float *scores, void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * Fine-grained attribution (Sec. 6 "Finer grains"; App. "Experimental details", the
+ * fine-grained probe): the variance contribution of each retained row j to each query head h,
+ *     kappa_hj = (1 - pi_j) / pi_j^2 * a_hj^2 |v_j - yhat_h|^2 / Nhat_h^2
+ * (the summand of Theorem 2, so sum_j kappa_hj = vhat_h), summed over the unit's query heads
+ * and over the rows whose original position idxc[j] falls in each block of block_rows
+ * positions:  blocks[u * nblocks + b] = sum_h sum_{j: idxc_j / block_rows = b} kappa_hj.
+ * Evicted blocks ranked by this sum are the retrieval targets of the paper's probe.
+ *   q, Kc, Vc, pic, idxc, count: as given to / written by ebd_attend_certify and ebd_evict;
+ *   y, lse: the outputs of ebd_attend_certify for the same q (yhat and ln Nhat).
+ *   Rows with pi = 1, with idxc < 0 (appended decode rows) or past the last block add nothing.
+ *   block_rows >= 1; 1 <= nblocks <= 8192; max_rows as for ebd_attend_certify (rows of a unit
+ *   beyond it are ignored).  blocks [U, nblocks] fp32 is written.  No workspace.
+ */
+typedef struct ebd_blocks_params {
+    int32_t num_units;
+    int32_t group;
+    int32_t head_dim;
+    int32_t block_rows;
+    int64_t nblocks;
+    int64_t max_rows;
+    const int64_t *cap_off;
+    float scale;
+} ebd_blocks_params;
+
+ebd_status ebd_block_contributions(const ebd_blocks_params *p, const uint16_t *q,
+                                   const uint16_t *Kc, const uint16_t *Vc, const float *pic,
+                                   const int32_t *idxc, const int32_t *count, const float *y,
+                                   const float *lse, float *blocks, void *stream);
+
+/*
+ * Deployed certificate, one decode step (App. "Experimental details": eq. (4) at delta = 0.1 on
+ * every fourth head of every layer over the first six decode steps, averaged, then maximized
+ * over the steps).  For every sequence s: the mean of radius[u, g] over the units with
+ * unit_seq[u] = s and the query heads g whose index (unit_head0[u] + g) is a multiple of
+ * head_stride; cert[s] = max(cert[s], mean) (the caller sets cert before the first step);
+ * mean_out[s] (or NULL) receives the mean.  A sequence without sampled pairs keeps cert[s]
+ * and gets mean 0.  unit_seq [U] device int32 (negative: not counted); unit_head0 [U] device
+ * int32 or NULL (all 0); radius [U, G] as written by ebd_attend_certify.
+ */
+typedef struct ebd_cert_params {
+    int32_t num_units;
+    int32_t group;
+    int32_t num_seqs;
+    int32_t head_stride;
+    const int32_t *unit_seq;
+    const int32_t *unit_head0;
+} ebd_cert_params;
+
+ebd_status ebd_certificate_step(const ebd_cert_params *p, const float *radius, float *cert,
+                                float *mean_out, void *stream);
+
 /* which-values for ebd_workspace_size */
 #define EBD_WS_EVICT 0
 #define EBD_WS_ATTEND 1
@@ -254,7 +306,7 @@ const char *ebd_version(void);
  * bracketed by HIP events recorded on the launch stream.  ebd_timing_read() waits for the
  * recorded events, and adds the elapsed times of kernel `name` ("evict_select",
  * "evict_copy", "attend_split", "attend_finalize", "append_certain", "scores_stats",
- * "scores_accum") to *total_ms and
+ * "scores_accum", "block_contrib", "cert_step") to *total_ms and
  * its launch count to *launches; it then clears that kernel's record.  Not meant for use
  * from several host threads at once.
  */

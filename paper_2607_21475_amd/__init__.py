@@ -104,6 +104,30 @@ class ebd_scores_params(ctypes.Structure):
     ]
 
 
+class ebd_blocks_params(ctypes.Structure):
+    _fields_ = [
+        ("num_units", ctypes.c_int32),
+        ("group", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_rows", ctypes.c_int32),
+        ("nblocks", ctypes.c_int64),
+        ("max_rows", ctypes.c_int64),
+        ("cap_off", ctypes.c_void_p),
+        ("scale", ctypes.c_float),
+    ]
+
+
+class ebd_cert_params(ctypes.Structure):
+    _fields_ = [
+        ("num_units", ctypes.c_int32),
+        ("group", ctypes.c_int32),
+        ("num_seqs", ctypes.c_int32),
+        ("head_stride", ctypes.c_int32),
+        ("unit_seq", ctypes.c_void_p),
+        ("unit_head0", ctypes.c_void_p),
+    ]
+
+
 _P = ctypes.c_void_p
 _lib.ebd_evict.argtypes = [ctypes.POINTER(ebd_evict_params)] + [_P] * 12 + [ctypes.c_size_t, _P]
 _lib.ebd_evict.restype = ctypes.c_int
@@ -112,6 +136,10 @@ _lib.ebd_attend_certify.argtypes = [ctypes.POINTER(ebd_attend_params)] + [_P] * 
 _lib.ebd_attend_certify.restype = ctypes.c_int
 _lib.ebd_scores.argtypes = [ctypes.POINTER(ebd_scores_params)] + [_P] * 4 + [ctypes.c_size_t, _P]
 _lib.ebd_scores.restype = ctypes.c_int
+_lib.ebd_block_contributions.argtypes = [ctypes.POINTER(ebd_blocks_params)] + [_P] * 10
+_lib.ebd_block_contributions.restype = ctypes.c_int
+_lib.ebd_certificate_step.argtypes = [ctypes.POINTER(ebd_cert_params)] + [_P] * 4
+_lib.ebd_certificate_step.restype = ctypes.c_int
 _lib.ebd_append_certain.argtypes = [ctypes.c_int32, ctypes.c_int32] + [_P] * 11
 _lib.ebd_append_certain.restype = ctypes.c_int
 _lib.ebd_workspace_size.argtypes = [ctypes.c_int32, _P]
@@ -264,6 +292,38 @@ def ebd_scores(params: ebd_scores_params, q, K, scores, workspace, stream=None) 
                            _ptr(scores, torch.float32, "scores"), _ptr(workspace, None, "workspace"),
                            workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ebd_scores", code)
+
+
+def ebd_block_contributions(num_units, group, nblocks, max_rows, cap_off, q, Kc, Vc, pic, idxc,
+                            count, y, lse, blocks, block_rows=64, scale=0.0, stream=None) -> None:
+    """Per-block variance contributions of the retained rows (asynchronous)."""
+    p = ebd_blocks_params()
+    p.num_units, p.group, p.head_dim = int(num_units), int(group), HEAD_DIM
+    p.block_rows, p.nblocks, p.max_rows = int(block_rows), int(nblocks), int(max_rows)
+    p.cap_off = _ptr(cap_off, torch.int64, "cap_off")
+    p.scale = float(scale)
+    bf, f32 = torch.bfloat16, torch.float32
+    code = _lib.ebd_block_contributions(ctypes.byref(p), _ptr(q, bf, "q"), _ptr(Kc, bf, "Kc"),
+                                        _ptr(Vc, bf, "Vc"), _ptr(pic, f32, "pic"),
+                                        _ptr(idxc, torch.int32, "idxc"),
+                                        _ptr(count, torch.int32, "count"), _ptr(y, f32, "y"),
+                                        _ptr(lse, f32, "lse"), _ptr(blocks, f32, "blocks"),
+                                        _stream(stream))
+    _check("ebd_block_contributions", code)
+
+
+def ebd_certificate_step(num_units, group, num_seqs, unit_seq, radius, cert, mean_out=None,
+                         head_stride=4, unit_head0=None, stream=None) -> None:
+    """Fold one decode step's mean sampled radius into the running certificate."""
+    p = ebd_cert_params()
+    p.num_units, p.group, p.num_seqs, p.head_stride = int(num_units), int(group), int(num_seqs), int(head_stride)
+    p.unit_seq = _ptr(unit_seq, torch.int32, "unit_seq")
+    p.unit_head0 = _ptr(unit_head0, torch.int32, "unit_head0")
+    f32 = torch.float32
+    code = _lib.ebd_certificate_step(ctypes.byref(p), _ptr(radius, f32, "radius"),
+                                     _ptr(cert, f32, "cert"), _ptr(mean_out, f32, "mean_out"),
+                                     _stream(stream))
+    _check("ebd_certificate_step", code)
 
 
 def ebd_append_certain(num_units, cap_off, count, k_new, v_new, Kc, Vc, pic, idxc=None,

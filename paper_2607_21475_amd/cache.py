@@ -16,23 +16,26 @@ from . import (EBD_F_NO_OFFSET, EBD_WS_ATTEND, EBD_WS_EVICT, EBD_WS_SCORES, HEAD
                scores_params, workspace)
 
 
-def unit_capacity(n: int, budget_frac: float, n_prot: int, extra: int = 0, align: int = 16) -> int:
+def unit_capacity(n: int, budget_frac: float, n_prot: int, extra: int = 0, align: int = 16,
+                  pi_min: float = 0.01) -> int:
     """Rows reserved for one unit's retained set.
 
-    The retained count is |P| plus a sum of independent Bernoullis with mean m = f n - |P| and
-    variance at most m, so f n + 8 sqrt(m) + 16 rows make an overflow negligible (it is still
+    The retained count is |P| plus a sum of independent Bernoullis whose mean is the tail
+    budget m = f n - |P|, or pi_min |T| when the floor alone exceeds it, and whose variance is
+    at most that mean; mean + 8 sqrt(mean) + 16 rows make an overflow negligible (it is still
     detected and flagged by the kernels).  `extra` reserves rows for appended decode tokens.
     """
     if n <= 0:
         return ((extra + align - 1) // align) * align
-    m = max(budget_frac * n - n_prot, 0.0)
-    c = budget_frac * n + 8.0 * math.sqrt(m + 1.0) + 16
+    n_tail = max(n - n_prot, 0)
+    tail = max(budget_frac * n - n_prot, pi_min * n_tail, 0.0)
+    c = n_prot + tail + 8.0 * math.sqrt(tail + 1.0) + 16
     c = min(int(math.ceil(c)), n) + extra
     return ((c + align - 1) // align) * align
 
 
 def plan_capacity(lengths: Sequence[int], budgets: Union[float, Sequence[float]], n_sink: int,
-                  n_recent: int, extra: int = 0):
+                  n_recent: int, extra: int = 0, pi_min: float = 0.01):
     """Host list of cap_off [U+1] for the given unit lengths and budget fractions."""
     U = len(lengths)
     if isinstance(budgets, (int, float)):
@@ -40,7 +43,7 @@ def plan_capacity(lengths: Sequence[int], budgets: Union[float, Sequence[float]]
     off = [0]
     for n, f in zip(lengths, budgets):
         n_prot = min(int(n), n_sink + n_recent)
-        off.append(off[-1] + unit_capacity(int(n), float(f), n_prot, extra))
+        off.append(off[-1] + unit_capacity(int(n), float(f), n_prot, extra, pi_min=pi_min))
     return off
 
 
@@ -73,7 +76,7 @@ def evict(K: torch.Tensor, V: torch.Tensor, scores: torch.Tensor, seq_off: torch
     U = len(lengths)
     if cap_off_host is None:
         budgets = budget_frac if budget_per_unit is None else budget_per_unit.tolist()
-        cap_off_host = plan_capacity(lengths, budgets, n_sink, n_recent, extra_rows)
+        cap_off_host = plan_capacity(lengths, budgets, n_sink, n_recent, extra_rows, pi_min)
     caps = [b - a for a, b in zip(cap_off_host[:-1], cap_off_host[1:])]
     rows = cap_off_host[-1]
     cap_off = torch.tensor(cap_off_host, dtype=torch.int64, device=dev)

@@ -342,6 +342,69 @@ ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint1
   return EBD_OK;
 }
 
+ebd_status ebd_block_contributions(const ebd_blocks_params *p, const uint16_t *q,
+                                   const uint16_t *Kc, const uint16_t *Vc, const float *pic,
+                                   const int32_t *idxc, const int32_t *count, const float *y,
+                                   const float *lse, float *blocks, void *stream) {
+  if (!p) return EBD_ERR_INVALID_ARG;
+  if (p->num_units < 0 || p->group < 1 || p->block_rows < 1 || p->nblocks < 1 ||
+      p->nblocks > kMaxBlocks || p->max_rows < 0 || p->scale < 0.0f || !std::isfinite(p->scale))
+    return EBD_ERR_INVALID_ARG;
+  if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  if (p->num_units == 0) return EBD_OK;
+  if (!p->cap_off || !q || !Kc || !Vc || !pic || !idxc || !count || !y || !lse || !blocks)
+    return EBD_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(y, 8))
+    return EBD_ERR_INVALID_ARG;
+  const ebd_status ds = check_device();
+  if (ds != EBD_OK) return ds;
+  BlocksLaunch L;
+  L.U = p->num_units;
+  L.G = p->group;
+  L.block_rows = p->block_rows;
+  L.nblocks = p->nblocks;
+  L.max_rows = p->max_rows;
+  L.cap_off = p->cap_off;
+  L.count = count;
+  L.q = q;
+  L.Kc = Kc;
+  L.Vc = Vc;
+  L.pic = pic;
+  L.idxc = idxc;
+  L.y = y;
+  L.lse = lse;
+  L.scale = p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)kHeadDim);
+  L.blocks = blocks;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (timed("block_contrib", s, [&] { return launch_block_contrib(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  return EBD_OK;
+}
+
+ebd_status ebd_certificate_step(const ebd_cert_params *p, const float *radius, float *cert,
+                                float *mean_out, void *stream) {
+  if (!p || p->num_units < 0 || p->group < 1 || p->num_seqs < 0 || p->head_stride < 1)
+    return EBD_ERR_INVALID_ARG;
+  if (p->num_seqs == 0) return EBD_OK;
+  if (!cert || (p->num_units > 0 && (!p->unit_seq || !radius))) return EBD_ERR_INVALID_ARG;
+  const ebd_status ds = check_device();
+  if (ds != EBD_OK) return ds;
+  CertLaunch L;
+  L.U = p->num_units;
+  L.G = p->group;
+  L.S = p->num_seqs;
+  L.head_stride = p->head_stride;
+  L.unit_seq = p->unit_seq;
+  L.unit_head0 = p->unit_head0;
+  L.radius = radius;
+  L.cert = cert;
+  L.mean_out = mean_out;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (timed("cert_step", s, [&] { return launch_cert_step(L, s); }) != hipSuccess)
+    return EBD_ERR_HIP;
+  return EBD_OK;
+}
+
 ebd_status ebd_append_certain(int32_t num_units, int32_t head_dim, const int64_t *cap_off,
                               int32_t *count, const uint16_t *k_new, const uint16_t *v_new,
                               const int32_t *pos_new, uint16_t *Kc, uint16_t *Vc, float *pic,

@@ -109,6 +109,28 @@ struct ScoresLaunch {
   float2 *stats;        // [U, nsplit, W] (max, exp-sum) per split and query
 };
 
+struct BlocksLaunch {
+  int32_t U, G, block_rows;
+  int64_t nblocks, max_rows;
+  const int64_t *cap_off;
+  const int32_t *count;
+  const uint16_t *q, *Kc, *Vc;
+  const float *pic;
+  const int32_t *idxc;
+  const float *y, *lse;
+  float scale;
+  float *blocks;  // [U, nblocks]
+};
+
+struct CertLaunch {
+  int32_t U, G, S, head_stride;
+  const int32_t *unit_seq, *unit_head0;
+  const float *radius;
+  float *cert, *mean_out;
+};
+
+constexpr int64_t kMaxBlocks = 8192;  // blocks per unit of ebd_block_contributions (LDS bins)
+
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows);
 size_t scores_workspace_bytes(int32_t U, int32_t nsplit, int32_t W);
 
@@ -119,5 +141,7 @@ hipError_t launch_attend_finalize(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_append_certain(const AppendLaunch &L, hipStream_t s);
 hipError_t launch_scores_stats(const ScoresLaunch &L, hipStream_t s);
 hipError_t launch_scores_accum(const ScoresLaunch &L, hipStream_t s);
+hipError_t launch_block_contrib(const BlocksLaunch &L, hipStream_t s);
+hipError_t launch_cert_step(const CertLaunch &L, hipStream_t s);
 
 }  // namespace ebd

@@ -21,8 +21,8 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     for fn in ("ebd_evict", "ebd_attend_certify", "ebd_append_certain", "ebd_scores",
-               "ebd_workspace_size", "ebd_status_string", "ebd_version", "ebd_timing_enable",
-               "ebd_timing_read"):
+               "ebd_block_contributions", "ebd_certificate_step", "ebd_workspace_size",
+               "ebd_status_string", "ebd_version", "ebd_timing_enable", "ebd_timing_read"):
         assert fn in names, fn
 
 
@@ -193,6 +193,32 @@ def test_scores_argument_validation_and_workspace():
     assert lib.ebd_workspace_size(ebd.EBD_WS_SCORES, ctypes.byref(p)) == ws(8, 86, 7)
 
 
+def test_finegrain_argument_validation():
+    ebd, lib = _lib()
+
+    def bp(**kw):
+        p = ebd.ebd_blocks_params()
+        p.num_units, p.group, p.head_dim = kw.get("U", 4), kw.get("G", 7), kw.get("d", 128)
+        p.block_rows, p.nblocks, p.max_rows = kw.get("rows", 64), kw.get("nb", 96), 4096
+        p.cap_off = FAKE
+        return p
+
+    def call(p):
+        return lib.ebd_block_contributions(ctypes.byref(p), *([FAKE] * 9), FAKE, None)
+
+    assert call(bp(d=64)) == ebd.EBD_ERR_UNSUPPORTED
+    for bad in (dict(G=0), dict(rows=0), dict(nb=0), dict(nb=8193), dict(U=-1)):
+        assert call(bp(**bad)) == ebd.EBD_ERR_INVALID_ARG, bad
+    assert call(bp(U=0)) == ebd.EBD_OK
+    c = ebd.ebd_cert_params()
+    c.num_units, c.group, c.num_seqs, c.head_stride, c.unit_seq = 4, 7, 2, 0, FAKE
+    assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, FAKE, None, None) == ebd.EBD_ERR_INVALID_ARG
+    c.head_stride = 4
+    assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, None, None, None) == ebd.EBD_ERR_INVALID_ARG
+    c.num_seqs = 0
+    assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, FAKE, None, None) == ebd.EBD_OK
+
+
 def test_binding_requires_gpu_tensors():
     torch = pytest.importorskip("torch")
     ebd, lib = _lib()
@@ -208,3 +234,23 @@ def test_no_oracle_in_product_path():
             if f.endswith((".py", ".hip", ".cpp", ".hpp", ".h")):
                 src = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in src.lower(), f
+
+
+def test_capacity_plan_covers_floor_and_protected():
+    """The planned capacity covers the protected positions plus the expected tail (the budget
+    m, or pi_min |T| when the floor exceeds it) with room for its spread."""
+    from paper_2607_21475_amd import cache
+
+    # budget below the protected count: the floor alone keeps pi_min of the tail
+    c = cache.unit_capacity(300, 0.1, 68, pi_min=0.01)
+    assert c >= 68 + 0.01 * 232 + 8 and c % 16 == 0
+    c = cache.unit_capacity(300, 0.1, 68, pi_min=0.2)
+    assert c >= 68 + 0.2 * 232 + 8 * (0.2 * 232) ** 0.5
+    # the usual case: f n + 8 sqrt(m) + 16, rounded up to 16, never above n (+ extra rows)
+    c = cache.unit_capacity(6144, 0.25, 68)
+    m = 0.25 * 6144 - 68
+    assert c == int(-(-(0.25 * 6144 + 8 * (m + 1) ** 0.5 + 16) // 16) * 16)
+    assert cache.unit_capacity(100, 1.0, 68, extra=5) == 112  # min(n, ...) + 5, aligned
+    assert cache.unit_capacity(0, 0.5, 0, extra=3) == 16
+    off = cache.plan_capacity([300, 0, 6144], [0.1, 0.5, 0.25], 4, 64)
+    assert off[0] == 0 and off[1] >= 80 and off[2] == off[1] and off[3] > off[2]

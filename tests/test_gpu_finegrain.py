@@ -1,0 +1,95 @@
+"""GPU parity of the fine-grained attribution and the deployed certificate step (through the
+C ABI) against the fp64 oracle.
+
+Bars: block contributions within 1e-3 relative of the oracle's, given the GPU's own yhat and
+ln Nhat (plus 1e-7 of the unit's largest block); the blocks of a unit sum to its summed vhat
+within 1e-2 relative; certificate means and running maxima within 1e-6 relative.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import paper_2607_21475_amd  # noqa: F401  (fails loudly if libebd.so is missing)
+    yield
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+@pytest.mark.parametrize("lengths,G,budget,block_rows", [
+    ([4096] * 6, 7, 0.25, 64),
+    ([6144, 0, 300, 9000], 4, 0.1, 64),
+    ([3000, 1500], 12, 0.3, 128),          # two head blocks, added in order
+])
+def test_block_contributions(lengths, G, budget, block_rows):
+    _say("block contributions lengths=%s G=%d" % (lengths, G))
+    import paper_2607_21475_amd as ebd
+    from paper_2607_21475_amd import cache
+
+    K, V, seq_off = synth.make_cache(lengths, seed=41, device="cuda")
+    sc = synth.window_scores(K, seq_off, seed=42)
+    q = synth.make_queries(len(lengths), G, seed=43, device="cuda")
+    out = cache.evict(K, V, sc, seq_off, lengths, budget_frac=budget, seed=2)
+    res = cache.attend_certify(out, q)
+    U = len(lengths)
+    nb = (max(lengths) + block_rows - 1) // block_rows
+    blocks = torch.empty((U, nb), dtype=torch.float32, device="cuda")
+    ebd.ebd_block_contributions(U, G, nb, out.max_cap, out.cap_off, q, out.Kc, out.Vc, out.pic,
+                                out.idxc, out.count, res["y"], res["lse"], blocks,
+                                block_rows=block_rows)
+    torch.cuda.synchronize()
+    coff, cnt = _np(out.cap_off), _np(out.count)
+    got = _np(blocks).astype(np.float64)
+    vh = _np(res["vhat"]).astype(np.float64)
+    bits = synth.bf16_bits
+    assert not (_np(out.status) & oracle.ST_CAP_OVERFLOW).any()
+    for u in range(U):
+        a, c = coff[u], int(min(cnt[u], coff[u + 1] - coff[u]))
+        ref = oracle.block_contributions(bits(q[u]), bits(out.Kc[a:a + c]), bits(out.Vc[a:a + c]),
+                                         _np(out.pic[a:a + c]), _np(out.idxc[a:a + c]),
+                                         _np(res["y"][u]).astype(np.float64),
+                                         _np(res["lse"][u]).astype(np.float64), nb, block_rows)
+        tol = 1e-3 * np.abs(ref) + 1e-7 * max(ref.max(initial=0.0), 1e-30)
+        assert np.all(np.abs(got[u] - ref) <= tol), (u, np.max(np.abs(got[u] - ref) / (np.abs(ref) + 1e-30)))
+        if c > 0:
+            assert abs(got[u].sum() - vh[u].sum()) <= 1e-2 * vh[u].sum() + 1e-30
+
+
+def test_certificate_step_over_decode_steps():
+    _say("certificate step")
+    import paper_2607_21475_amd as ebd
+
+    rng = np.random.default_rng(5)
+    U, G, S = 28 * 4 * 4, 7, 4  # 28 layers x 4 sequences x 4 KV heads, 7 query heads each
+    unit_seq = np.repeat(np.tile(np.arange(S), 28), 4).astype(np.int32)
+    unit_head0 = np.tile(np.arange(4) * G, 28 * S).astype(np.int32)
+    cert = torch.zeros(S, dtype=torch.float32, device="cuda")
+    mean = torch.zeros(S, dtype=torch.float32, device="cuda")
+    us = torch.as_tensor(unit_seq, device="cuda")
+    h0 = torch.as_tensor(unit_head0, device="cuda")
+    ref_cert = np.zeros(S)
+    for step in range(6):
+        r = rng.gamma(2.0, 0.1 * (step + 1), (U, G)).astype(np.float32)
+        ebd.ebd_certificate_step(U, G, S, us, torch.as_tensor(r, device="cuda"), cert, mean,
+                                 head_stride=4, unit_head0=h0)
+        ref_cert, ref_mean = oracle.certificate_step(r, unit_seq, S, 4, unit_head0, ref_cert)
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(_np(mean), ref_mean, rtol=1e-6)
+        np.testing.assert_allclose(_np(cert), ref_cert, rtol=1e-6)
