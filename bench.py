@@ -123,6 +123,9 @@ def main() -> int:
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/hbm_traffic_<workload>.json from rocprofv3 --pmc csv runs")
     ap.add_argument("--pmc-command", default="", help="command recorded in the summary")
+    ap.add_argument("--compare-arms", action="store_true",
+                    help="instead of timing: errors of the sampling designs against full attention")
+    ap.add_argument("--compare-units", type=int, default=256)
     args = ap.parse_args()
 
     if args.summarize_pmc:
@@ -146,6 +149,8 @@ def main() -> int:
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
     budgets = [float(b) for b in args.budgets.split(",")] if args.budgets else list(wl.budgets)
+    if args.compare_arms:
+        return compare_arms(args, wl, budgets)
     U, n, G = wl.units, wl.context, wl.group
     lengths = [n] * U
 
@@ -348,6 +353,100 @@ def main() -> int:
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+def compare_arms(args, wl, budgets) -> int:
+    """Relative error of each sampling design against full attention on a sample of units, and
+    the certificate's coverage; then the value-permutation demonstration for top-k: permuting
+    the evicted values leaves every retained-set statistic of top-k unchanged while its true
+    error moves (comparative only; synthetic caches stand in for the paper's models)."""
+    import torch
+
+    import paper_2607_21475_amd as ebd
+    import synth
+    from paper_2607_21475_amd import cache
+
+    U = min(args.compare_units, wl.units)
+    n, G = wl.context, wl.group
+    inp = synth.make_workload_inputs(wl, units=U, seed=args.seed, device="cuda")
+    lengths = [n] * U
+    kw = dict(n_sink=wl.n_sink, n_recent=wl.n_recent, pi_min=wl.pi_min, seed=args.seed)
+
+    def full_output(V):
+        full = cache.evict(inp["K"], V, inp["scores"], inp["seq_off"], lengths, budget_frac=1.0, **kw)
+        return cache.attend_certify(full, inp["q"])["y"]
+
+    def rel_err(y, yref):
+        return (torch.linalg.norm(y - yref, dim=2) / torch.linalg.norm(yref, dim=2)).flatten()
+
+    yref = full_output(inp["V"])
+    arms = (("poisson_hajek", ebd.EBD_DESIGN_POISSON, True),
+            ("poisson_no_offset", ebd.EBD_DESIGN_POISSON, False),
+            ("systematic_hajek", ebd.EBD_DESIGN_SYSTEMATIC, True),
+            ("topk", ebd.EBD_DESIGN_TOPK, True),
+            ("uniform_hajek", ebd.EBD_DESIGN_UNIFORM, True))
+    table = []
+    for b in budgets:
+        row = {"budget": b}
+        for name, design, offset in arms:
+            rc = cache.evict(inp["K"], inp["V"], inp["scores"], inp["seq_off"], lengths,
+                             budget_frac=b, design=design, **kw)
+            res = cache.attend_certify(rc, inp["q"], offset=offset)
+            err = rel_err(res["y"], yref)
+            ent = {"median_rel_err": round(float(err.median()), 5),
+                   "mean_retained": round(float(rc.count.float().mean()), 1)}
+            if design != ebd.EBD_DESIGN_TOPK:
+                r = res["r"].flatten()
+                ent["coverage"] = round(float((err <= r).float().mean()), 4)
+                ent["median_radius"] = round(float(r.median()), 5)
+                ent["spearman_radius_error"] = round(_spearman(r, err), 4)
+            row[name] = ent
+        table.append(row)
+
+    # Theorem 1 by construction: permute each unit's evicted value rows (top-k at the first budget)
+    b = budgets[0]
+    rc = cache.evict(inp["K"], inp["V"], inp["scores"], inp["seq_off"], lengths, budget_frac=b,
+                     design=ebd.EBD_DESIGN_TOPK, **kw)
+    y_top = cache.attend_certify(rc, inp["q"])["y"]
+    cnt = rc.count.cpu().tolist()
+    coff = rc.cap_off.cpu().tolist()
+    idx = rc.idxc.cpu()
+    g = torch.Generator(device="cpu")
+    g.manual_seed(args.seed + 99)
+    errs, same = [], True
+    for world in range(6):
+        perm = torch.arange(U * n)
+        for u in range(U):
+            kept = torch.zeros(n, dtype=torch.bool)
+            kept[idx[coff[u]:coff[u] + cnt[u]].long()] = True
+            ev = torch.nonzero(~kept).flatten() + u * n
+            perm[ev] = ev[torch.randperm(ev.numel(), generator=g)]
+        Vp = inp["V"][perm.to("cuda")]
+        rc2 = cache.evict(inp["K"], Vp, inp["scores"], inp["seq_off"], lengths, budget_frac=b,
+                          design=ebd.EBD_DESIGN_TOPK, **kw)
+        y2 = cache.attend_certify(rc2, inp["q"])["y"]
+        rows = torch.cat([torch.arange(coff[u], coff[u] + cnt[u]) for u in range(U)]).to("cuda")
+        same = (same and bool(torch.equal(y2, y_top)) and bool(torch.equal(rc2.count, rc.count))
+                and bool(torch.equal(rc2.idxc[rows], rc.idxc[rows]))
+                and bool(torch.equal(rc2.Vc[rows], rc.Vc[rows])))
+        errs.append(float(rel_err(y_top, full_output(Vp)).median()))
+    line = {"mode": "compare_arms", "workload": wl.name, "units": U, "group": G, "context": n,
+            "data": "synthetic (seeded); the paper's models and prompts are not used",
+            "arms": table,
+            "topk_value_permutation": {"budget": b, "worlds": 6,
+                                       "median_rel_err_per_world": [round(e, 5) for e in errs],
+                                       "max_over_min": round(max(errs) / max(min(errs), 1e-30), 3),
+                                       "retained_set_and_output_identical": same}}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def _spearman(a, b) -> float:
+    ra = a.argsort().argsort().double()
+    rb = b.argsort().argsort().double()
+    ra -= ra.mean()
+    rb -= rb.mean()
+    return float((ra * rb).sum() / (ra.norm() * rb.norm() + 1e-300))
 
 
 def cpu_baseline(inp, plans, wl, args, torch):
