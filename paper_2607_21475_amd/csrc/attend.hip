@@ -16,9 +16,10 @@
 //   MFMA (16x16x32 bf16, exact products, fp32 sums): A = K tile (16 rows x 32 dims per k-block,
 //   loaded straight from HBM in operand layout), B = [q_0 .. q_{GB-1}, q_0 .. q_{GB-1}, 0 ..]
 //   (16 columns).  Each lane then holds 4 rows x 1 column of logits; columns < GB become weights
-//   w, columns GB..2GB-1 (same logits) become variance weights c.  f32 16x16x4 MFMAs then form
+//   w, columns GB..2GB-1 (same logits) become variance weights c.  bf16 16x16x32 MFMAs then form
 //   o = sum w v (rows < GB) and Cv = sum c v (rows GB..2GB-1) together, with V in its natural
-//   row-major layout (no transpose, exact fp32 products).
+//   row-major layout (no transpose): each fp32 weight enters as an exact three-term bf16 sum,
+//   so every product is exact and only the fp32 sums round.
 //   Range-term candidates: every weight lane keeps its four largest g^2 |v|^2 (g^2 = (1 - pi) w^2)
 //   among its rows, plus the maxima of g^2 |v|^2 and of g^2 over what it dropped; the split's
 //   record holds those 16 candidates per head, their largest |v| and the non-candidate maxima.
@@ -92,7 +93,8 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
                                                    sacc, 0, 0, 0);
   // log2 pi of the 4 rows of this row group: quad lane i computes row i, the quad shares it.
   const int qi = __lane_id() & 3;
-  const float pq = qi == 0 ? T.p[0] : (qi == 1 ? T.p[1] : (qi == 2 ? T.p[2] : T.p[3]));
+  const float p01 = (qi & 1) ? T.p[1] : T.p[0], p23 = (qi & 1) ? T.p[3] : T.p[2];
+  const float pq = (qi & 2) ? p23 : p01;  // selects, not an indexed (scratch) array
   const float lq = plain ? 0.0f : fast_log2(pq);  // the uncorrected pass drops the offset
   float lp[4];
   lp[0] = dpp_f<0x00>(lq);  // quad_perm [0,0,0,0]
@@ -130,17 +132,16 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
     S.mrun = mnew;
   }
 
-  float vf[4][8], nv2[4];
+  // |v|^2 of the lane's 4 rows (exact fp32 products)
+  float nv2[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const uint32_t w4[4] = {T.v[j][0], T.v[j][1], T.v[j][2], T.v[j][3]};
     float sq = 0.0f;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      vf[j][2 * k] = bf16_lo(w4[k]);
-      vf[j][2 * k + 1] = bf16_hi(w4[k]);
-      sq = fmaf(vf[j][2 * k], vf[j][2 * k], sq);
-      sq = fmaf(vf[j][2 * k + 1], vf[j][2 * k + 1], sq);
+      const float a = bf16_lo(T.v[j][k]), b = bf16_hi(T.v[j][k]);
+      sq = fmaf(a, a, sq);
+      sq = fmaf(b, b, sq);
     }
     nv2[j] = row16_sum(sq);
   }
@@ -158,11 +159,36 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
     gsq[i] = cc;
     kap[i] = cc * nv2[i];
   }
+  // o and Cv on bf16 MFMAs (16x16x32), exactly: every fp32 weight is split into three bf16
+  // terms hi + mid + lo (successive 8-bit pieces of its significand, each difference exact), and
+  // V (bf16) times each term is an exact product, so only the fp32 summation rounds.  The
+  // contraction runs over this row group's 4 rows x {hi, mid} in one MFMA and 4 rows x {lo, 0}
+  // in a second, against each V element taken twice.  Lane (g, c) holds rows 4g + j at dims
+  // 8c .. 8c + 7 of V, which is the B operand for dims 8c + e, e = 0..7.
+  u32x4 whm, wlo;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t hb = __float_as_uint(val[i]) & 0xffff0000u;
+    const float r = val[i] - __uint_as_float(hb);  // exact: the low 16 significand bits
+    const uint32_t mb = __float_as_uint(r) & 0xffff0000u;
+    const float lo = r - __uint_as_float(mb);  // exact, and exact in bf16
+    whm[i] = (hb >> 16) | mb;
+    wlo[i] = __float_as_uint(lo) >> 16;
+  }
 #pragma unroll
-    for (int db = 0; db < 8; ++db)
-      S.acc[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(val[j], vf[j][db], S.acc[db], 0, 0, 0);
+  for (int e = 0; e < 8; ++e) {
+    u32x4 bop;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t x = T.v[j][e >> 1];
+      bop[j] = __builtin_amdgcn_perm(x, x, (e & 1) ? 0x03020302u : 0x01000100u);  // element twice
+    }
+    S.acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, whm),
+                                                      __builtin_bit_cast(bf16x8, bop), S.acc[e], 0,
+                                                      0, 0);
+    S.acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wlo),
+                                                      __builtin_bit_cast(bf16x8, bop), S.acc[e], 0,
+                                                      0, 0);
   }
 
   // Range-term candidates: weight lanes take the rows of even tiles, variance lanes (same
