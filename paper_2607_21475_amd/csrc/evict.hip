@@ -2,7 +2,10 @@
 // Sec. 3.1: evicted rows are deleted, retained rows keep one stored pi each).
 //
 // Two launches per call:
-//   evict_select  one work-group (4 waves) per unit.  Stages the unit's scores in LDS (up to
+//   evict_select_reg (units of at most 6144 tokens) one work-group of 2 waves per unit, the scores
+//                 in registers, so that every unit of a large batch is resident at once; the same
+//                 steps as evict_select below with one barrier per reduction or prefix.
+//   evict_select  (longer units) one work-group (4 waves) per unit.  Stages the unit's scores in LDS (up to
 //                 16384 tokens, protected positions marked by a negative sentinel; longer units
 //                 are re-read from memory), solves lambda with sum_T clip(lambda s, eps, 1) = m by
 //                 safeguarded Newton steps on the piecewise linear g(lambda) (exact once the
@@ -103,6 +106,137 @@ __device__ __forceinline__ uint64_t points_below(uint64_t C, uint32_t s) {
 // Integer weight of a stored pi: ceil(pi 2^32), the Poisson test's exact threshold.
 __device__ __forceinline__ uint64_t pi_weight(float pi) {
   return (uint64_t)ceilf(pi * 4294967296.0f);
+}
+
+// Tail statistics of a unit: |T|, positive scores, their sum, the largest score and the smallest
+// positive one.
+struct TailStats {
+  double n_tail, n_pos, s_sum;
+  float s_max, s_minp;
+};
+
+// lambda of eq. (2) with sum_T clip(lambda s, eps, 1) = m, plus the status bits of the boundary
+// cases.  `pass(lf, H, L, S)` gives the unit's totals at lambda = lf: tail positions with
+// lf s >= 1 (H), with lf s <= eps (L), and the sum of the scores in between (S).
+// g(lambda) = H + eps L + lambda S is piecewise linear and nondecreasing: a Newton step on the
+// current piece is exact once the piece is right, and the bracket [lo, hi] with
+// g(lo) < m <= g(hi) guards every step (bisection when a step leaves it).
+template <class Pass>
+__device__ double solve_lambda(const TailStats &T, double m, float eps, int pi_mode, uint32_t &st,
+                               Pass &&pass) {
+  if (T.n_tail == 0.0) return 0.0;
+  if (pi_mode == 1) {
+    if (m <= (double)eps * T.n_tail) st |= EBD_ST_BUDGET_FLOOR;
+    return (T.s_sum > 0.0 && m > 0.0) ? m / T.s_sum : 0.0;
+  }
+  if (m <= (double)eps * T.n_tail) {
+    st |= EBD_ST_BUDGET_FLOOR;
+    return 0.0;
+  }
+  if (m >= T.n_pos + (double)eps * (T.n_tail - T.n_pos)) {
+    st |= EBD_ST_NO_EVICTION;
+    return INFINITY;
+  }
+  double lo = (double)eps / (double)T.s_max;
+  double hi = 1.0 / (double)T.s_minp;
+  double cur = fmin(fmax(m / T.s_sum, lo), hi);
+  double pH = -1.0, pL = -1.0, pS = -1.0;
+  bool from_newton = false;
+  for (int it = 0; it < 96; ++it) {
+    const float lf = (float)cur;
+    double dH, dL, dS;
+    pass(lf, dH, dL, dS);
+    if (from_newton && dH == pH && dL == pL && dS == pS) break;  // same piece: cur is exact
+    const double g = dH + (double)eps * dL + (double)lf * dS;
+    if (g < m) lo = (double)lf;
+    else hi = (double)lf;
+    if (g == m) break;
+    double nxt = dS > 0.0 ? (m - dH - (double)eps * dL) / dS : -1.0;
+    from_newton = (nxt > lo && nxt < hi);
+    if (!from_newton) nxt = 0.5 * (lo + hi);
+    if ((float)nxt == lf || hi - lo <= 1e-9 * hi) {
+      cur = from_newton ? nxt : cur;
+      break;
+    }
+    pH = dH;
+    pL = dL;
+    pS = dS;
+    cur = nxt;
+  }
+  return cur;
+}
+
+// Top-k threshold: the k-th largest key among the tail keys (score bits, which order like the
+// non-negative cleaned scores), by radix select 8 bits per pass from the top over a histogram in
+// LDS.  `count(prefix, pmask, shift)` adds to hist every tail key whose bits under pmask equal
+// prefix, at digit (key >> shift) & 255.  Returns the key; `left` gets how many tail positions
+// equal to it belong to the k largest.  Every thread of the NT-thread block calls it.
+template <int NT, class Count>
+__device__ uint32_t radix_kth(int k, int *hist, int *sel, int (*wtot)[NT / 64], int &left,
+                              Count &&count) {
+  constexpr int DPT = 256 / NT;  // digits per thread, descending with the thread index
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  uint32_t prefix = 0, pmask = 0;
+  int krem = k, buf = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int d = t; d < 256; d += NT) hist[d] = 0;
+    __syncthreads();
+    count(prefix, pmask, shift);
+    __syncthreads();
+    int c[DPT], mine = 0;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+      c[e] = hist[255 - DPT * t - e];
+      mine += c[e];
+    }
+    int incl = mine;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) wtot[buf][wv] = incl;
+    __syncthreads();
+    for (int w = 0; w < wv; ++w) incl += wtot[buf][w];
+    buf ^= 1;
+    int before = incl - mine;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+      if (before < krem && krem <= before + c[e]) {  // the digit holding the krem-th largest key
+        sel[0] = 255 - DPT * t - e;
+        sel[1] = krem - before;
+      }
+      before += c[e];
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sel[0] << shift;
+    pmask |= 255u << shift;
+    krem = sel[1];
+    __syncthreads();
+  }
+  left = krem;
+  return prefix;
+}
+
+// Top-k size and threshold from the tail count: k = floor(m + 1/2) clipped to [0, |T|].  With
+// 0 < k < |T| the radix select gives the threshold key and how many positions equal to it to
+// keep; k = |T| keeps every tail key (threshold +0.0, no limit); k = 0 keeps none.
+template <int NT, class Count>
+__device__ uint32_t topk_threshold(double m, double n_tail, int *hist, int *sel,
+                                   int (*wtot)[NT / 64], int &tleft, uint32_t &st, Count &&count) {
+  int64_t k = (int64_t)floor(m + 0.5);
+  if (k < 0) k = 0;
+  if (k >= (int64_t)n_tail) {
+    k = (int64_t)n_tail;
+    if (n_tail > 0.0) st |= EBD_ST_NO_EVICTION;
+  }
+  if (k > 0 && k < (int64_t)n_tail) return radix_kth<NT>((int)k, hist, sel, wtot, tleft, count);
+  if (k > 0) {
+    tleft = INT32_MAX;
+    return 0u;
+  }
+  tleft = 0;
+  return 0xffffffffu;
 }
 
 }  // namespace
@@ -220,124 +354,47 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
   }
   uint32_t st = bad ? EBD_ST_BAD_SCORE : 0u;
 
-  const double n_zero = n_tail - n_pos;
-  double lam = 0.0;
   const bool topk = L.design == EBD_DESIGN_TOPK;
-  // Top-k: k = floor(m + 1/2) tail positions; tkey is the k-th largest key (score bits, which
-  // order like the non-negative scores) and tleft how many positions equal to it to keep.
-  int64_t k_top = 0;
+  // Top-k: tkey is the k-th largest tail key and tleft how many positions equal to it to keep.
   uint32_t tkey = 0xffffffffu;
   int tleft = 0;
   if (topk) {
-    k_top = (int64_t)floor(m + 0.5);
-    if (k_top < 0) k_top = 0;
-    if (k_top >= (int64_t)n_tail) {
-      k_top = (int64_t)n_tail;
-      if (n_tail > 0.0) st |= EBD_ST_NO_EVICTION;
-    }
-    if (k_top > 0 && k_top < (int64_t)n_tail) {
-      // radix select over the cleaned tail scores, 8 bits per pass from the top
-      uint32_t prefix = 0, pmask = 0;
-      int krem = (int)k_top;
-      for (int shift = 24; shift >= 0; shift -= 8) {
-        s_hist[t] = 0;  // kSelectThreads == 256 bins
-        __syncthreads();
-        for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
-          const float4 s4 = group(gi);
-          const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+    tkey = topk_threshold<kSelectThreads>(
+        m, n_tail, s_hist, s_sel, s_tot, tleft, st, [&](uint32_t prefix, uint32_t pmask, int shift) {
+          for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
+            const float4 s4 = group(gi);
+            const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t key = __float_as_uint(sv[j]);
-            if (sv[j] >= 0.0f && (key & pmask) == prefix)
-              atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t key = __float_as_uint(sv[j]);
+              if (sv[j] >= 0.0f && (key & pmask) == prefix)
+                atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+            }
           }
-        }
-        __syncthreads();
-        // counts from the top digit down: thread t holds digit 255 - t
-        const int hv = s_hist[255 - t];
-        int incl = hv;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(incl, o);
-          if (lane >= o) incl += y;
-        }
-        if (lane == 63) s_tot[rbuf][wv] = incl;
-        __syncthreads();
-        for (int w = 0; w < wv; ++w) incl += s_tot[rbuf][w];
-        rbuf ^= 1;
-        if (incl >= krem && incl - hv < krem) {  // the digit holding the krem-th largest key
-          s_sel[0] = 255 - t;
-          s_sel[1] = krem - (incl - hv);
-        }
-        __syncthreads();
-        prefix |= (uint32_t)s_sel[0] << shift;
-        pmask |= 255u << shift;
-        krem = s_sel[1];
-        __syncthreads();
-      }
-      tkey = prefix;
-      tleft = krem;
-    } else if (k_top == (int64_t)n_tail) {
-      tkey = 0u;  // every tail key (+0.0 and up) is at or above it: keep all
-      tleft = INT32_MAX;
-    }
+        });
   }
-  if (topk || n_tail == 0.0) {
-    lam = 0.0;
-  } else if (L.pi_mode == 1) {
-    lam = (s_sum > 0.0 && m > 0.0) ? m / s_sum : 0.0;
-    if (m <= (double)eps * n_tail) st |= EBD_ST_BUDGET_FLOOR;
-  } else if (m <= (double)eps * n_tail) {
-    lam = 0.0;
-    st |= EBD_ST_BUDGET_FLOOR;
-  } else if (m >= n_pos + (double)eps * n_zero) {
-    lam = INFINITY;
-    st |= EBD_ST_NO_EVICTION;
-  } else {
-    // g(lam) = H + eps L + lam S_mid is piecewise linear and nondecreasing.  A Newton step on
-    // the current piece is exact once the piece is right; the bracket [lo, hi] with
-    // g(lo) < m <= g(hi) guards every step.
-    double lo = (double)eps / (double)s_max;
-    double hi = 1.0 / (double)s_minp;
-    double cur = fmin(fmax(m / s_sum, lo), hi);
-    double pH = -1.0, pL = -1.0, pS = -1.0;
-    bool from_newton = false;
-    for (int it = 0; it < 96; ++it) {
-      const float lf = (float)cur;
-      float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
-      for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
-        const float4 s4 = group(gi);
-        const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+  const TailStats ts{n_tail, n_pos, s_sum, s_max, s_minp};
+  const double lam =
+      topk ? 0.0
+           : solve_lambda(ts, m, eps, L.pi_mode, st, [&](float lf, double &dH, double &dL, double &dS) {
+               float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
+               for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
+                 const float4 s4 = group(gi);
+                 const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float p = lf * sv[j];
-          const bool in = sv[j] >= 0.0f;
-          H += (in && p >= 1.0f) ? 1.0f : 0.0f;
-          Lo += (in && p <= eps) ? 1.0f : 0.0f;
-          Sm += (in && p > eps && p < 1.0f) ? sv[j] : 0.0f;
-        }
-      }
-      double dH = H, dL = Lo, dS = Sm;
-      block_sum3(dH, dL, dS, R, rbuf);
-      if (from_newton && dH == pH && dL == pL && dS == pS) break;  // same piece: cur is exact
-      const double g = dH + (double)eps * dL + (double)lf * dS;
-      if (g < m) lo = (double)lf;
-      else hi = (double)lf;
-      if (g == m) break;
-      double nxt = dS > 0.0 ? (m - dH - (double)eps * dL) / dS : -1.0;
-      from_newton = (nxt > lo && nxt < hi);
-      if (!from_newton) nxt = 0.5 * (lo + hi);
-      if ((float)nxt == lf || hi - lo <= 1e-9 * hi) {
-        cur = from_newton ? nxt : cur;
-        break;
-      }
-      pH = dH;
-      pL = dL;
-      pS = dS;
-      cur = nxt;
-    }
-    lam = cur;
-  }
+                 for (int j = 0; j < 4; ++j) {
+                   const float p = lf * sv[j];
+                   const bool in = sv[j] >= 0.0f;
+                   H += (in && p >= 1.0f) ? 1.0f : 0.0f;
+                   Lo += (in && p <= eps) ? 1.0f : 0.0f;
+                   Sm += (in && p > eps && p < 1.0f) ? sv[j] : 0.0f;
+                 }
+               }
+               dH = H;
+               dL = Lo;
+               dS = Sm;
+               block_sum3(dH, dL, dS, R, rbuf);
+             });
   const float lamf = (float)lam;
 
   // Mask and in-order write of the retained rows' pi and positions: 1024-token blocks, ranks
@@ -486,6 +543,361 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
 }
 
 // ---------------------------------------------------------------------------------------------
+// evict_select_reg: the same selection for units of at most 512 G4 tokens (G4 <= 12, so up to
+// 6144 tokens; longer units take evict_select), two waves per unit
+// with the scores in registers (G4 groups of 4 tokens per thread; group gi = 128 q + thread, so
+// loads are coalesced and positions ascend with (q, wave, lane, j)).  Without LDS staging every
+// unit of a large batch is resident at once.  Each reduction or prefix costs one barrier: the
+// mask bits of the whole unit are drawn first, then one exchange of the per-(q, wave) counts
+// gives every retained row its output slot.
+// ---------------------------------------------------------------------------------------------
+template <int G4>
+__global__ __launch_bounds__(kSelectRegThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void evict_select_reg_kernel(EvictLaunch L) {
+  constexpr int NT = kSelectRegThreads, NW = NT / 64;
+  __shared__ double s_d[2][NW][3];
+  __shared__ float s_f[NW][2];
+  __shared__ int s_i[NW][3];
+  __shared__ int s_cnt[G4][NW];
+  __shared__ unsigned long long s_c64[G4][NW];
+  __shared__ int s_hist[256];
+  __shared__ int s_sel[2];
+  __shared__ int s_wtot[2][NW];
+  const int u = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int64_t base = L.seq_off[u];
+  const int64_t n64 = L.seq_off[u + 1] - base;
+  const int64_t cbase = L.cap_off[u];
+  const int64_t cap = L.cap_off[u + 1] - cbase;
+  if (n64 > L.max_rows || n64 > 512 * G4 || cap > (int64_t)L.copy_blocks * kCopyRows) {
+    if (t == 0) {
+      L.count[u] = 0;
+      L.status[u] = EBD_ST_BAD_LAYOUT;
+      if (L.lambda_out) L.lambda_out[u] = 0.0f;
+    }
+    return;
+  }
+  const int n = (int)n64;
+  const int64_t nprot = min(n64, (int64_t)L.n_sink + (int64_t)L.n_recent);
+  const double f = L.budget_per_unit ? (double)L.budget_per_unit[u] : (double)L.budget_frac;
+  const double m = f * (double)n - (double)nprot;
+  const float eps = L.pi_min;
+  // T = [tail_lo, tail_hi), as 32-bit positions (the unit has at most 512 G4 tokens)
+  const int tail_lo = (int)min((int64_t)L.n_sink, n64);
+  const int tail_hi = (int)max(n64 - (int64_t)L.n_recent, (int64_t)0);
+  const int design = L.design;
+  const bool uniform = design == EBD_DESIGN_UNIFORM;  // tail scores taken as 1, not read
+  const bool topk = design == EBD_DESIGN_TOPK;
+  const bool vec = ((base & 3) == 0);
+  const float *sc = L.scores + base;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int rb = 0;
+
+  // Unit totals of two wave-uniform counts and a per-lane fp32 partial (summed in fp64); all
+  // threads get them.
+  auto bsum = [&](int a, int b, float c, double &A, double &B, double &C) {
+    const double cw = wave_sum((double)c);
+    if (lane == 0) {
+      s_d[rb][wv][0] = (double)a;
+      s_d[rb][wv][1] = (double)b;
+      s_d[rb][wv][2] = cw;
+    }
+    __syncthreads();
+    A = B = C = 0.0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      A += s_d[rb][w][0];
+      B += s_d[rb][w][1];
+      C += s_d[rb][w][2];
+    }
+    rb ^= 1;
+  };
+
+  // Scores: cleaned tail scores, -1 outside the tail (protected or past the end); every position
+  // is checked for bad values, protected ones included.
+  float sv[G4][4];
+  int n_tail = 0, n_pos = 0, n_bad = 0;  // wave totals (ballots)
+  float s_sum = 0.0f, s_max = 0.0f, s_minp = INFINITY;
+  {
+    // raw buffer loads bounded by the unit: positions past its end read 0
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(sc, (uint32_t)(4 * n));
+    float4 raw[G4];
+    if (uniform) {
+#pragma unroll
+      for (int q = 0; q < G4; ++q) raw[q] = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+    } else if (vec) {
+#pragma unroll
+      for (int q = 0; q < G4; ++q)
+        raw[q] = __builtin_bit_cast(
+            float4, __builtin_amdgcn_raw_buffer_load_b128(rs, 16u * (uint32_t)(q * NT + t), 0, 0));
+    } else {
+#pragma unroll
+      for (int q = 0; q < G4; ++q) {
+        const uint32_t off = 16u * (uint32_t)(q * NT + t);
+        raw[q].x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+        raw[q].y = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4, 0, 0));
+        raw[q].z = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off + 8, 0, 0));
+        raw[q].w = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off + 12, 0, 0));
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < G4; ++q) {
+      const float rv[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = 4 * (q * NT + t) + j;
+        uint32_t b = 0;
+        const float c = clean_score(rv[j], b);
+        const bool tail = i < n && i >= tail_lo && i < tail_hi;
+        sv[q][j] = tail ? c : -1.0f;
+        n_bad += __popcll(__ballot(i < n && b));
+        n_tail += __popcll(__ballot(tail));
+        n_pos += __popcll(__ballot(tail && c > 0.0f));
+        s_sum += tail ? c : 0.0f;
+        s_max = fmaxf(s_max, tail ? c : 0.0f);
+        s_minp = fminf(s_minp, (tail && c > 0.0f) ? c : INFINITY);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // one group at a time: bounded register pressure
+    }
+  }
+  // From here on a slot's class is read from its value alone: hiding how it was formed keeps
+  // the compiler from carrying 48 per-slot lane masks through every phase instead.
+#pragma unroll
+  for (int q = 0; q < G4; ++q)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(sv[q][j]));
+  double d_tail, d_pos, d_sum;
+  {
+    s_max = wave_max(s_max);
+    s_minp = wave_min(s_minp);
+    if (lane == 0) {
+      s_i[wv][0] = n_bad;
+      s_f[wv][0] = s_max;
+      s_f[wv][1] = s_minp;
+    }
+    bsum(n_tail, n_pos, s_sum, d_tail, d_pos, d_sum);  // its barrier also publishes s_i, s_f
+    n_bad = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      n_bad += s_i[w][0];
+      s_max = fmaxf(s_max, s_f[w][0]);
+      s_minp = fminf(s_minp, s_f[w][1]);
+    }
+    n_tail = (int)d_tail;
+  }
+  const uint32_t bad = n_bad > 0 ? 1u : 0u;
+  uint32_t st = bad ? EBD_ST_BAD_SCORE : 0u;
+
+  uint32_t tkey = 0xffffffffu;
+  int tleft = 0;
+  if (topk) {
+    tkey = topk_threshold<NT>(m, (double)n_tail, s_hist, s_sel, s_wtot, tleft, st,
+                              [&](uint32_t prefix, uint32_t pmask, int shift) {
+#pragma unroll
+                                for (int q = 0; q < G4; ++q)
+#pragma unroll
+                                  for (int j = 0; j < 4; ++j) {
+                                    const uint32_t key = __float_as_uint(sv[q][j]);
+                                    if (sv[q][j] >= 0.0f && (key & pmask) == prefix)
+                                      atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+                                  }
+                              });
+  }
+  // Slots outside the tail hold -1: lf (-1) <= eps counts them in L, so L is corrected by their
+  // number (every slot of the unit's G4 x 4 x NT is one or the other).
+  const double n_out = (double)(4 * G4 * NT) - (double)n_tail;
+  const TailStats ts{d_tail, d_pos, d_sum, s_max, s_minp};
+  const double lam =
+      topk ? 0.0
+           : solve_lambda(ts, m, eps, L.pi_mode, st, [&](float lf, double &dH, double &dL, double &dS) {
+               int H = 0, Lo = 0;  // wave totals (ballots)
+               float Sm = 0.0f;
+#pragma unroll
+               for (int q = 0; q < G4; ++q)
+#pragma unroll
+                 for (int j = 0; j < 4; ++j) {
+                   const float p = lf * sv[q][j];
+                   const bool hb = p >= 1.0f, lb = p <= eps;
+                   H += __popcll(__ballot(hb));
+                   Lo += __popcll(__ballot(lb));
+                   Sm += (hb || lb) ? 0.0f : sv[q][j];
+                 }
+               bsum(H, Lo, Sm, dH, dL, dS);
+               dL -= n_out;
+             });
+  float lamf = (float)lam;
+
+  // pi of slot (q, j): 1 outside the tail; the clipped lambda s in the tail (top-k: 1 or 0 by
+  // the keep bit).
+  auto slot_pi = [&](int q, int j, bool keep) -> float {
+    if (!(sv[q][j] >= 0.0f)) return 1.0f;
+    if (topk) return keep ? 1.0f : 0.0f;
+    return token_pi(true, sv[q][j], lamf, eps);
+  };
+  // The per-slot range tests are taken again in each phase: kept as lane masks across the
+  // phases they would crowd the scalar registers.
+  int nn = n, tb = 4 * t;  // this thread's first position, as an opaque value
+  asm volatile("" : "+s"(nn), "+v"(tb));
+  uint64_t keep = 0;  // bit 4 q + j
+  const uint64_t sd = L.seed_per_unit ? L.seed_per_unit[u] : L.seed;
+  if (design == EBD_DESIGN_SYSTEMATIC) {
+    // integer weights ceil(pi 2^32) in position order against one start per unit; the wave
+    // scans are taken twice (totals, then prefixes) rather than kept across the exchange
+    const uint32_t start =
+        philox4x32_10(make_uint4(0u, (uint32_t)u, L.epoch, kSystematicTag), (uint32_t)sd,
+                      (uint32_t)(sd >> 32)).x;
+    auto weights = [&](int q, uint64_t (&a)[4]) {
+      uint64_t tsum = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a[j] = tb + 4 * NT * q + j < nn ? pi_weight(slot_pi(q, j, false)) : 0u;
+        tsum += a[j];
+      }
+      return tsum;
+    };
+#pragma unroll
+    for (int q = 0; q < G4; ++q) {
+      uint64_t a[4];
+      const uint64_t incl = wave_scan_u64(weights(q, a));
+      if (lane == 63) s_c64[q][wv] = incl;
+    }
+    __syncthreads();
+    asm volatile("" : "+v"(lamf));  // recompute pi here rather than keep every slot's value live
+    uint64_t acc = 0;
+#pragma unroll
+    for (int q = 0; q < G4; ++q) {
+      uint64_t a[4];
+      const uint64_t tsum = weights(q, a);
+      uint64_t C = acc + wave_scan_u64(tsum) - tsum;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const uint64_t c = s_c64[q][w];
+        C += w < wv ? c : 0u;
+        acc += c;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint64_t Cn = C + a[j];
+        if (a[j] != 0u && points_below(Cn, start) != points_below(C, start))
+          keep |= 1ull << (4 * q + j);
+        C = Cn;
+      }
+    }
+  } else if (topk) {
+    // tail positions at the threshold key are kept in position order while tleft lasts; the
+    // ballots are taken twice (totals, then ranks) rather than kept across the exchange
+    auto eq_ballot = [&](int q, int j) {
+      return __ballot(sv[q][j] >= 0.0f && __float_as_uint(sv[q][j]) == tkey);
+    };
+#pragma unroll
+    for (int q = 0; q < G4; ++q) {
+      int etot = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) etot += __popcll(eq_ballot(q, j));
+      if (lane == 0) s_cnt[q][wv] = etot;
+    }
+    __syncthreads();
+    int acc = 0;
+#pragma unroll
+    for (int q = 0; q < G4; ++q) {
+      int er = acc;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) er += __popcll(eq_ballot(q, j) & below);
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const int c = s_cnt[q][w];
+        er += w < wv ? c : 0;
+        acc += c;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (!(sv[q][j] >= 0.0f)) {
+          if (tb + 4 * NT * q + j < nn) keep |= 1ull << (4 * q + j);  // protected
+          continue;
+        }
+        const uint32_t key = __float_as_uint(sv[q][j]);
+        bool sel = key > tkey;
+        if (key == tkey) sel = er++ < tleft;
+        if (sel) keep |= 1ull << (4 * q + j);
+      }
+    }
+    __syncthreads();  // s_cnt is reused for the output ranks
+  } else {
+#pragma unroll
+    for (int q = 0; q < G4; ++q) {
+      const int gi = (tb >> 2) + NT * q;  // group index: positions 4 gi .. 4 gi + 3
+      if (4 * gi >= nn) continue;
+      const uint4 x = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)u, L.epoch, kPhiloxTag),
+                                    (uint32_t)sd, (uint32_t)(sd >> 32));
+      const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (4 * gi + j < nn && keep_token(xw[j], slot_pi(q, j, false)))
+          keep |= 1ull << (4 * q + j);
+    }
+  }
+
+  // Output slots: per-(q, wave) retained counts, one exchange, then every retained row writes its
+  // pi and position; the unit's full pi vector on request.
+#pragma unroll
+  for (int q = 0; q < G4; ++q) {
+    int wtot = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) wtot += __popcll(__ballot((keep >> (4 * q + j)) & 1ull));
+    if (lane == 0) s_cnt[q][wv] = wtot;
+  }
+  __syncthreads();
+  asm volatile("" : "+v"(lamf), "+v"(tb));  // as above: recomputed per slot for the output
+  // buffer stores: a slot at or past the capacity (or a dropped row, sent past it) writes nothing
+  const uint32_t capw = (uint32_t)min(cap, (int64_t)INT32_MAX / 4);
+  const __amdgpu_buffer_rsrc_t rpi = make_rsrc(L.pic + cbase, 4u * capw);
+  const __amdgpu_buffer_rsrc_t rix = make_rsrc(L.idxc + cbase, 4u * capw);
+  const __amdgpu_buffer_rsrc_t rfull = make_rsrc(L.pi_full ? L.pi_full + base : nullptr,
+                                                 L.pi_full ? 4u * (uint32_t)n : 0u);
+  int total = 0;  // running count of the rows before block q, then the unit's count
+#pragma unroll
+  for (int q = 0; q < G4; ++q) {
+    int r = total;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r += __popcll(__ballot((keep >> (4 * q + j)) & 1ull) & below);
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const int c = s_cnt[q][w];
+      r += w < wv ? c : 0;
+      total += c;
+    }
+    float pv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool kj = (keep >> (4 * q + j)) & 1ull;
+      pv[j] = slot_pi(q, j, kj);
+      const uint32_t off = kj ? 4u * (uint32_t)r : 0xfffffff0u;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, pv[j]), rpi, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32((uint32_t)(tb + 4 * NT * q + j), rix, off, 0, 0);
+      r += kj ? 1 : 0;
+    }
+    if (L.pi_full) {
+      if (vec) {
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(u32x4, make_float4(pv[0], pv[1], pv[2], pv[3])), rfull,
+            4u * (uint32_t)(tb + 4 * NT * q), 0, 0);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, pv[j]), rfull,
+                                                4u * (uint32_t)(tb + 4 * NT * q + j), 0, 0);
+      }
+    }
+  }
+  if (t == 0) {
+    if (total > cap) st |= EBD_ST_CAP_OVERFLOW;
+    L.count[u] = total;
+    L.status[u] = st;
+    if (L.lambda_out) L.lambda_out[u] = lamf;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // evict_copy: gather the retained K and V rows in order
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kCopyThreads) void evict_copy_kernel(EvictLaunch L) {
@@ -534,8 +946,16 @@ __global__ __launch_bounds__(kCopyThreads) void evict_copy_kernel(EvictLaunch L)
 }
 
 hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s) {
-  const size_t lds = L.stage_rows > 0 ? (size_t)((L.stage_rows + 3) / 4) * 16 : 0;
-  hipLaunchKernelGGL(evict_select_kernel, dim3(L.U), dim3(kSelectThreads), lds, s, L);
+  const dim3 grid((unsigned)L.U), reg(kSelectRegThreads);
+  const int64_t g4 = (L.max_rows + 511) / 512;  // groups of 4 tokens per thread (two waves)
+  if (g4 <= 2) hipLaunchKernelGGL(evict_select_reg_kernel<2>, grid, reg, 0, s, L);
+  else if (g4 <= 4) hipLaunchKernelGGL(evict_select_reg_kernel<4>, grid, reg, 0, s, L);
+  else if (g4 <= 8) hipLaunchKernelGGL(evict_select_reg_kernel<8>, grid, reg, 0, s, L);
+  else if (g4 <= 12) hipLaunchKernelGGL(evict_select_reg_kernel<12>, grid, reg, 0, s, L);
+  else {
+    const size_t lds = L.stage_rows > 0 ? (size_t)((L.stage_rows + 3) / 4) * 16 : 0;
+    hipLaunchKernelGGL(evict_select_kernel, grid, dim3(kSelectThreads), lds, s, L);
+  }
   return hipGetLastError();
 }
 

@@ -102,6 +102,10 @@ def _check_evict(lengths, K, V, seq_off, sc, out, n_sink=4, n_recent=64, budget=
     ([6144] * 6, 0.25),                       # 3 chunks per unit
     ([0, 1, 5, 70, 100, 777, 2047, 2048, 2049, 4096, 5000, 6144, 9000, 16384], 0.2),  # ragged
     ([20000, 40001, 3], 0.1),                 # longer than 16384: streamed scores
+    # units of at most 6144 tokens: scores held in registers, 2 to 12 groups per thread
+    ([0, 1, 5, 70, 100, 777, 2047, 2048, 2049, 4096, 5000, 6144], 0.2),
+    ([1, 3, 511, 512, 513, 1024], 0.3),
+    ([2000, 17, 1500], 0.15),
 ])
 def test_evict_parity(lengths, budget):
     _say("evict parity lengths=%s budget=%s" % (lengths[:6], budget))
@@ -196,6 +200,8 @@ def test_evict_deterministic():
     ([4096] * 8, 0.10),
     ([0, 1, 5, 70, 100, 777, 2047, 2048, 2049, 5000, 16384], 0.25),
     ([20000, 40001, 3], 0.1),                 # streamed scores
+    ([0, 1, 5, 70, 777, 2049, 5000, 6144], 0.25),   # scores in registers
+    ([1024, 9], 0.2),
 ])
 def test_evict_systematic_design(lengths, budget):
     _say("evict systematic lengths=%s budget=%s" % (lengths[:6], budget))
@@ -217,6 +223,8 @@ def test_evict_systematic_design(lengths, budget):
     ([0, 1, 5, 70, 777, 2048, 5000, 16384], 0.3, True),   # integer scores: many ties
     ([20000, 40001, 3], 0.1, True),                       # streamed scores
     ([3000, 3000], 1.0, False),                           # k = |T|: keep everything
+    ([0, 1, 5, 70, 777, 2048, 5000, 6144], 0.3, True),    # scores in registers
+    ([900, 1024], 0.05, False),
 ])
 def test_evict_topk_design(lengths, budget, ties):
     _say("evict top-k lengths=%s budget=%s ties=%s" % (lengths[:6], budget, ties))
@@ -242,9 +250,12 @@ def test_evict_topk_design(lengths, budget, ties):
         np.testing.assert_array_equal(_bits(out.Vc)[a:a + k], ref["Vc"][a:a + k])
 
 
-def test_evict_uniform_design():
-    lengths = [4096, 333, 6144, 20000]
-    _say("evict uniform")
+@pytest.mark.parametrize("lengths", [
+    [4096, 333, 6144, 20000],   # streamed scores
+    [4096, 333, 6144],          # scores in registers
+])
+def test_evict_uniform_design(lengths):
+    _say("evict uniform lengths=%s" % lengths)
     K, V, seq_off, sc, _ = _inputs(lengths, seed=23)
     sc = sc.clone()
     sc[5] = float("nan")  # not read by the uniform design: no flag
