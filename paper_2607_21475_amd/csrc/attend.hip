@@ -735,11 +735,32 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   }
 }
 
-// attend_finalize: one wave per (unit, head block) when units are cut into several splits; the
-// split records are combined into LDS, then finalized like a fused split.
+// attend_finalize: one wave per (unit, head block) when units are cut into several splits.  The
+// split records are combined into LDS, the candidate blocks of every split copied there too when
+// they fit (kFinStageBytes), then the unit is finalized like a fused split.  Every global read of
+// the records is issued in batches, so the wave waits on a handful of round trips rather than
+// one per candidate.
+constexpr size_t kFinStageBytes = 48 * 1024;
+
 template <int GB>
-__global__ __launch_bounds__(64) void attend_finalize_kernel(AttendLaunch L, int h0) {
-  extern __shared__ float s_fin[];
+__host__ __device__ constexpr size_t fin_stage_bytes(int32_t nsplit, int32_t nchunk) {
+  return (size_t)nsplit * GB * nchunk * kChunkFloats * sizeof(float);
+}
+// Float offsets in the finalize's LDS: the split scales after FinLds, the staged blocks after
+// them on a 16-byte boundary.
+template <int GB>
+__host__ __device__ constexpr size_t fin_scale_off() {
+  return FinLds<GB>::bytes() / sizeof(float);
+}
+template <int GB>
+__host__ __device__ constexpr size_t fin_stage_off(int32_t nsplit) {
+  return (fin_scale_off<GB>() + (size_t)nsplit * GB + 3) / 4 * 4;
+}
+
+template <int GB>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void attend_finalize_kernel(AttendLaunch L, int h0) {
+  extern __shared__ float s_fin[];  // FinLds, then the split scale factors, then staged blocks
   const int u = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t cbase = L.cap_off[u];
@@ -754,50 +775,108 @@ __global__ __launch_bounds__(64) void attend_finalize_kernel(AttendLaunch L, int
   const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h0) * L.rec;  // (s, h) at s G rec + h rec
   const int64_t sstride = (int64_t)L.G * L.rec;
   FinLds<GB> F(s_fin);
+  float *fsc = s_fin + fin_scale_off<GB>();           // [nsplit][GB]: scale of (s, h)
+  float *stage = s_fin + fin_stage_off<GB>(L.nsplit);  // [nsp][GB][nchunk][kChunkFloats]
+  const bool staged = fin_stage_bytes<GB>(L.nsplit, L.nchunk) <= kFinStageBytes;
 
-  // combined scalars: lane (h, s) pairs; M first, then the scaled sums
-  for (int h = 0; h < GB; ++h) {
-    float M = -INFINITY;
-    for (int s = lane; s < nsp; s += 64) M = fmaxf(M, rec0[s * sstride + h * L.rec + kRecM]);
-    M = wave_max(M);
-    float l = 0.0f, c0 = 0.0f, c2 = 0.0f;
-    for (int s = lane; s < nsp; s += 64) {
-      const float *r = rec0 + s * sstride + h * L.rec;
-      const float f = scale_of(r[kRecM], M);
-      l += f * r[kRecL];
-      c0 += f * f * r[kRecC0];
-      c2 += f * f * r[kRecC2];
+  // Scalars (M, l, C0, C2) of every (split, head): one float4 per lane and head, all in flight.
+  for (int s0 = 0; s0 < nsp; s0 += 64) {
+    const int sl = s0 + lane;
+    float4 r[GB];
+#pragma unroll
+    for (int h = 0; h < GB; ++h)
+      r[h] = sl < nsp ? *reinterpret_cast<const float4 *>(rec0 + sl * sstride + h * L.rec + kRecM)
+                      : make_float4(-INFINITY, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+    for (int h = 0; h < GB; ++h) {
+      if (sl < nsp) fsc[sl * GB + h] = r[h].x;  // the split's running max, for now
+      const float M = wave_max(r[h].x);
+      const float mo = s0 == 0 ? -INFINITY : F.hs[h * kHs + kHsM];  // earlier batches
+      const float Mn = fmaxf(M, mo);
+      const float f = scale_of(r[h].x, Mn);
+      float l = wave_sum(f * r[h].y), c0 = wave_sum(f * f * r[h].z), c2 = wave_sum(f * f * r[h].w);
+      if (lane == 0) {
+        const float fo = s0 == 0 ? 0.0f : scale_of(mo, Mn);
+        F.hs[h * kHs + kHsM] = Mn;
+        F.hs[h * kHs + kHsL] = l + (s0 == 0 ? 0.0f : fo * F.hs[h * kHs + kHsL]);
+        F.hs[h * kHs + kHsC0] = c0 + (s0 == 0 ? 0.0f : fo * fo * F.hs[h * kHs + kHsC0]);
+        F.hs[h * kHs + kHsC2] = c2 + (s0 == 0 ? 0.0f : fo * fo * F.hs[h * kHs + kHsC2]);
+      }
+      __syncthreads();
     }
-    l = wave_sum(l);
-    c0 = wave_sum(c0);
-    c2 = wave_sum(c2);
-    if (lane == 0) {
-      F.hs[h * kHs + kHsM] = M;
-      F.hs[h * kHs + kHsL] = l;
-      F.hs[h * kHs + kHsC0] = c0;
-      F.hs[h * kHs + kHsC2] = c2;
+  }
+  // the scale of every split to the combined max
+  for (int e = lane; e < nsp * GB; e += 64) fsc[e] = scale_of(fsc[e], F.hs[(e % GB) * kHs + kHsM]);
+  __syncthreads();
+
+  // o and Cv: two dims per lane, every slot of two splits in flight at once.
+  {
+    float2 acc[2 * GB];
+#pragma unroll
+    for (int slot = 0; slot < 2 * GB; ++slot) acc[slot] = make_float2(0.0f, 0.0f);
+    for (int sp = 0; sp < nsp; sp += 2) {
+      float2 a[2][2 * GB];
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int slot = 0; slot < 2 * GB; ++slot) {
+          const int h = slot < GB ? slot : slot - GB;
+          const int off = slot < GB ? kRecO : kRecCv;
+          a[q][slot] = sp + q < nsp ? reinterpret_cast<const float2 *>(
+                                          rec0 + (sp + q) * sstride + h * L.rec + off)[lane]
+                                    : make_float2(0.0f, 0.0f);
+        }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        if (sp + q >= nsp) break;
+#pragma unroll
+        for (int slot = 0; slot < 2 * GB; ++slot) {
+          const int h = slot < GB ? slot : slot - GB;
+          float f = fsc[(sp + q) * GB + h];
+          if (slot >= GB) f *= f;
+          acc[slot].x = fmaf(f, a[q][slot].x, acc[slot].x);
+          acc[slot].y = fmaf(f, a[q][slot].y, acc[slot].y);
+        }
+      }
+    }
+#pragma unroll
+    for (int slot = 0; slot < 2 * GB; ++slot)
+      reinterpret_cast<float2 *>(F.o + slot * kHeadDim)[lane] = acc[slot];
+  }
+
+  // Candidate blocks: every split's chunk blocks of these heads into LDS, 8 float4 per lane in
+  // flight (blocks of chunks a split does not have are copied too and never read).
+  const int per4 = L.nchunk * kChunkFloats / 4;  // float4 per (split, head)
+  if (staged) {
+    const int n4 = nsp * GB * per4;
+    float4 *dst = reinterpret_cast<float4 *>(stage);
+    for (int i0 = 0; i0 < n4; i0 += 8 * 64) {
+      float4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int i = min(i0 + 64 * k + lane, n4 - 1);  // past the end: a valid element, unused
+        const int sh = i / per4, o = i % per4;
+        v[k] = reinterpret_cast<const float4 *>(rec0 + (sh / GB) * sstride + (sh % GB) * L.rec +
+                                                kRecChunks)[o];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int i = i0 + 64 * k + lane;
+        if (i < n4) dst[i] = v[k];
+      }
     }
   }
   __syncthreads();
-  // combined o and Cv: slot-major, two dims per lane
-  for (int slot = 0; slot < 2 * GB; ++slot) {
-    const int h = slot < GB ? slot : slot - GB;
-    const int off = slot < GB ? kRecO : kRecCv;
-    const float M = F.hs[h * kHs + kHsM];
-    float2 acc = make_float2(0.0f, 0.0f);
-    for (int s = 0; s < nsp; ++s) {
-      const float *r = rec0 + s * sstride + h * L.rec;
-      float f = scale_of(r[kRecM], M);
-      if (slot >= GB) f *= f;
-      const float2 a = reinterpret_cast<const float2 *>(r + off)[lane];
-      acc.x += f * a.x;
-      acc.y += f * a.y;
-    }
-    reinterpret_cast<float2 *>(F.o + slot * kHeadDim)[lane] = acc;
-  }
-  __syncthreads();
-  const CandSrc C{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
+  const CandSrc C = staged ? CandSrc{stage, (int64_t)GB * per4 * 4, kChunkFloats, per4 * 4}
+                           : CandSrc{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
   finalize_block<GB>(L, u, h0, cnt, cbase, nsp, C, F);
+}
+
+template <int GB>
+size_t attend_finalize_lds(const AttendLaunch &L) {
+  const size_t b = fin_stage_off<GB>(L.nsplit) * sizeof(float);
+  const size_t st = fin_stage_bytes<GB>(L.nsplit, L.nchunk);
+  return st <= kFinStageBytes ? b + st : b;
 }
 
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows) {
@@ -827,6 +906,13 @@ size_t attend_split_lds(const AttendLaunch &L, int gb) {
   return b;
 }
 
+size_t attend_fused_lds_bytes(int32_t split_rows, int gb) {
+  AttendLaunch L{};
+  L.nsplit = 1;
+  L.nchunk = attend_chunks(split_rows);
+  return attend_split_lds(L, gb);
+}
+
 hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)L.U * L.nsplit)), block(kAttendThreads);
   for (int h0 = 0; h0 < L.G; h0 += kHeadBlock) {
@@ -853,14 +939,20 @@ hipError_t launch_attend_finalize(const AttendLaunch &L, hipStream_t s) {
   for (int h0 = 0; h0 < L.G; h0 += kHeadBlock) {
     const int gb = min(kHeadBlock, L.G - h0);
     switch (gb) {
-      case 1: hipLaunchKernelGGL(attend_finalize_kernel<1>, grid, block, FinLds<1>::bytes(), s, L, h0); break;
-      case 2: hipLaunchKernelGGL(attend_finalize_kernel<2>, grid, block, FinLds<2>::bytes(), s, L, h0); break;
-      case 3: hipLaunchKernelGGL(attend_finalize_kernel<3>, grid, block, FinLds<3>::bytes(), s, L, h0); break;
-      case 4: hipLaunchKernelGGL(attend_finalize_kernel<4>, grid, block, FinLds<4>::bytes(), s, L, h0); break;
-      case 5: hipLaunchKernelGGL(attend_finalize_kernel<5>, grid, block, FinLds<5>::bytes(), s, L, h0); break;
-      case 6: hipLaunchKernelGGL(attend_finalize_kernel<6>, grid, block, FinLds<6>::bytes(), s, L, h0); break;
-      case 7: hipLaunchKernelGGL(attend_finalize_kernel<7>, grid, block, FinLds<7>::bytes(), s, L, h0); break;
-      default: hipLaunchKernelGGL(attend_finalize_kernel<8>, grid, block, FinLds<8>::bytes(), s, L, h0); break;
+#define EBD_FIN(N)                                                                             \
+  case N:                                                                                      \
+    hipLaunchKernelGGL(attend_finalize_kernel<N>, grid, block, attend_finalize_lds<N>(L), s, L, \
+                       h0);                                                                    \
+    break;
+      EBD_FIN(1)
+      EBD_FIN(2)
+      EBD_FIN(3)
+      EBD_FIN(4)
+      EBD_FIN(5)
+      EBD_FIN(6)
+      EBD_FIN(7)
+      default: EBD_FIN(8)
+#undef EBD_FIN
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

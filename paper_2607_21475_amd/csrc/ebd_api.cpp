@@ -84,11 +84,18 @@ constexpr size_t kEvictWorkspace = 256;
 
 // Rows per split (a multiple of 16).  Unless the caller fixes it: one split per unit when there
 // are enough units for kSplitWaves waves, else units are cut into equal splits until there are;
-// splits stay within [kSplitMinRows, kSplitMaxRows] rows.
+// splits stay within [kSplitMinRows, kSplitMaxRows] rows.  When the units alone give enough
+// waves, a whole unit of up to kSplitRowsLimit rows stays one split (which then also finalizes
+// its unit, with no second launch) as long as that split's LDS still lets two waves share a SIMD.
 int32_t attend_split_rows(const ebd_attend_params *p) {
   if (p->split_rows > 0) return p->split_rows;
   const int64_t cap = p->max_rows > 0 ? p->max_rows : 1;
   const int64_t U = p->num_units > 0 ? p->num_units : 1;
+  const int32_t G = p->group > 0 ? p->group : 1;
+  const int64_t waves = U * ((G + kHeadBlock - 1) / kHeadBlock);
+  if (waves >= kSplitWaves && cap <= kSplitRowsLimit &&
+      attend_fused_lds_bytes((int32_t)cap, std::min(G, kHeadBlock)) <= kSplitLdsBudget)
+    return (int32_t)((cap + 15) / 16 * 16);
   int64_t ns = (kSplitWaves + U - 1) / U;
   ns = std::max<int64_t>(ns, (cap + kSplitMaxRows - 1) / kSplitMaxRows);
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, cap / kSplitMinRows));

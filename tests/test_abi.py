@@ -148,6 +148,11 @@ def test_workspace_sizes():
     assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 7) + 1024 * 287 * 7 * rec(48) * 4
     a.group = 12  # two head blocks
     assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 12) + 1024 * 287 * 12 * rec(48) * 4
+    # many units of up to 8192 rows stay one split while its LDS allows two waves per SIMD
+    a.split_rows, a.group, a.num_units, a.max_rows = 0, 4, 8192, 4720
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(8192, 4)
+    a.group = 8  # 8 heads: chunk blocks and finalize LDS exceed 20 KB, cut into 4096-row splits
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(8192, 8) + 8192 * 2 * 8 * rec(2368) * 4
     for bad in (40, 8208):  # not a multiple of 16; longer than a wave's candidate store
         a.split_rows = bad
         assert lib.ebd_workspace_size(ebd.EBD_WS_ATTEND, ctypes.byref(a)) == 0
