@@ -357,7 +357,6 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
   // (2) Candidate bounds: a candidate's value f g |v - yhat| / l is at most f g (Vmax + |yhat|)/l.
   //     Candidate e = ((s nchunk + k) GB + h) kCand + j.
   const int R = L.split_rows;
-  const int E = nsp * L.nchunk * GB * kCand;
   auto decode = [&](int e, int &h, int &row, float &fg, float &ub) -> bool {
     const int j = e % kCand;
     int r = e / kCand;
@@ -374,11 +373,50 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     ub = fg * (blk[kChVmax] + hs[kHsYn]);
     return true;
   };
-  for (int e = lane; e < E; e += 64) {
-    int h, row;
-    float fg, ub;
-    if (decode(e, h, row, fg, ub) && ub > 0.0f)
-      atomicMax(&F.best[h], ((unsigned long long)__float_as_uint(ub) << 32) | (unsigned)e);
+  // A chunk block x = (s nchunk + k) GB + h bounds all its candidates at once: candidate j's
+  // bound is g_j F_x with F_x = f (Vmax + |yhat|) / l, so the block's largest g decides.  One
+  // lane per block; per head, the largest bound (and its candidate) goes to F.best.
+  const int nx = nsp * L.nchunk * GB;
+  auto block_bound = [&](int x, int &h, int &jmax) -> float {  // 0 for a chunk that is absent
+    h = x % GB;
+    const int sk = x / GB, s = sk / L.nchunk, k = sk % L.nchunk;
+    jmax = 0;
+    if (k * kChunkRows >= min(cnt - s * R, R)) return 0.0f;
+    const float *blk = C.base + s * C.sstride + k * C.kstride + h * C.hstride;
+    float gmax = 0.0f;
+#pragma unroll 8
+    for (int j = 0; j < kCand; ++j) {
+      const float gj = blk[kChG + j];
+      if (gj > gmax) {
+        gmax = gj;
+        jmax = j;
+      }
+    }
+    const float *hs = F.hs + h * kHs;
+    return scale_of(blk[kChM], hs[kHsM]) * gmax / hs[kHsL] * (blk[kChVmax] + hs[kHsYn]);
+  };
+  {
+    unsigned long long key[GB];
+#pragma unroll
+    for (int h = 0; h < GB; ++h) key[h] = 0ull;
+    for (int x = lane; x < nx; x += 64) {
+      int h, j;
+      const float ub = block_bound(x, h, j);
+      const unsigned long long kk =
+          ub > 0.0f ? ((unsigned long long)__float_as_uint(ub) << 32) | (unsigned)(x * kCand + j) : 0ull;
+#pragma unroll
+      for (int hh = 0; hh < GB; ++hh) key[hh] = (hh == h && kk > key[hh]) ? kk : key[hh];
+    }
+#pragma unroll
+    for (int h = 0; h < GB; ++h) {
+      unsigned long long k = key[h];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long y = __shfl_xor(k, o);
+        k = y > k ? y : k;
+      }
+      if (lane == 0) F.best[h] = k;
+    }
   }
   __syncthreads();
 
@@ -444,24 +482,43 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     }
     __syncthreads();
   };
+  // Only blocks whose bound exceeds the head's best value are listed from, 32 lanes per block
+  // (with a relative margin, since the block bound rounds differently from a candidate's).
   int n = 0;
-  for (int e0 = 0; e0 < E; e0 += 64) {
-    const int e = e0 + lane;
-    int h = 0, row;
-    float fg, ub;
-    bool live = false;
-    if (e < E && decode(e, h, row, fg, ub))
-      live = ub > F.hs[h * kHs + kHsLb] && (unsigned)e != (unsigned)(F.best[h] & 0xffffffffull);
-    const uint64_t m = __ballot(live);
-    if (live) {
-      const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-      F.list[n + rank] = e;
+  for (int x0 = 0; x0 < nx; x0 += 64) {
+    bool liveb = false;
+    if (x0 + lane < nx) {
+      int h, j;
+      const float ub = block_bound(x0 + lane, h, j);
+      liveb = ub * 1.0001f > F.hs[h * kHs + kHsLb];
     }
-    n += (int)__popcll(m);
-    if (n > kListCap - 64) {
-      eval_list(n);
-      n = 0;
+    uint64_t mb = __ballot(liveb);
+    while (mb) {
+      const int xa = x0 + (int)__builtin_ctzll(mb);
+      mb &= mb - 1;
+      int xb = -1;
+      if (mb) {
+        xb = x0 + (int)__builtin_ctzll(mb);
+        mb &= mb - 1;
+      }
+      const int xx = lane < 32 ? xa : xb;
+      const int e = xx * kCand + (lane & 31);
+      int h = 0, row;
+      float fg, ub;
+      bool live = false;
+      if (xx >= 0 && decode(e, h, row, fg, ub))
+        live = ub > F.hs[h * kHs + kHsLb] && (unsigned)e != (unsigned)(F.best[h] & 0xffffffffull);
+      const uint64_t m = __ballot(live);
+      if (live) {
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        F.list[n + rank] = e;
+      }
+      n += (int)__popcll(m);
+      if (n > kListCap - 64) {
+        eval_list(n);
+        n = 0;
+      }
     }
   }
   if (n > 0) eval_list(n);
@@ -469,7 +526,6 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
   // (5) A chunk whose non-candidate bound f (A + B |yhat|) / l still exceeds the best value is
   //     rescanned row by row.
   const float scale2 = L.scale * kLog2e;
-  const int nx = nsp * L.nchunk * GB;
   bool qloaded = false;
   for (int x0 = 0; x0 < nx; x0 += 64) {
     const int x = x0 + lane;  // (s nchunk + k) GB + h
