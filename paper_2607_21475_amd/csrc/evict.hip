@@ -5,11 +5,12 @@
 //   evict_select_reg (units of at most 6144 tokens) one work-group of 2 waves per unit, the scores
 //                 in registers, so that every unit of a large batch is resident at once; the same
 //                 steps as evict_select below with one barrier per reduction or prefix.
-//   evict_select  (longer units) one work-group (4 waves) per unit.  Stages the unit's scores in LDS (up to
+//   evict_select  (longer units) one work-group per unit (8 waves while the scores are staged in
+//                 LDS, 4 when they are streamed).  Stages the unit's scores in LDS (up to
 //                 16384 tokens, protected positions marked by a negative sentinel; longer units
 //                 are re-read from memory), solves lambda with sum_T clip(lambda s, eps, 1) = m by
 //                 safeguarded Newton steps on the piecewise linear g(lambda) (exact once the
-//                 piece is found), then walks the unit in 1024-token blocks: Philox words and the
+//                 piece is found), then walks the unit in blocks of 4 tokens per thread: Philox words and the
 //                 exact retention test (Poisson), or a block scan of the integer weights
 //                 ceil(pi 2^32) against one start per unit (fixed-size systematic design), or
 //                 the score threshold of a radix select (top-k comparison design); ballot ranks
@@ -42,10 +43,11 @@ __device__ __forceinline__ float token_pi(bool tail, float s, float lam, float e
   return fminf(fmaxf(lam * s, eps), 1.0f);
 }
 
-// Block-wide sums over the 256 threads of evict_select (4 waves).  `buf` alternates between
-// calls so that one barrier per call suffices.
+// Block-wide reductions over the NW waves of evict_select.  `buf` alternates between calls so
+// that one barrier per call suffices.
+template <int NW>
 struct BlockRed {
-  double v[2][4][4];
+  double v[2][NW][4];
 };
 
 __device__ __forceinline__ double wave_sum_d(double x) {
@@ -54,7 +56,9 @@ __device__ __forceinline__ double wave_sum_d(double x) {
 }
 
 // Sums a, b, c (each exact in double for counts) over the block; all threads get the totals.
-__device__ __forceinline__ void block_sum3(double &a, double &b, double &c, BlockRed &R, int &buf) {
+template <int NW>
+__device__ __forceinline__ void block_sum3(double &a, double &b, double &c, BlockRed<NW> &R,
+                                           int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   a = wave_sum_d(a);
   b = wave_sum_d(b);
@@ -65,13 +69,17 @@ __device__ __forceinline__ void block_sum3(double &a, double &b, double &c, Bloc
     R.v[buf][wv][2] = c;
   }
   __syncthreads();
-  a = R.v[buf][0][0] + R.v[buf][1][0] + R.v[buf][2][0] + R.v[buf][3][0];
-  b = R.v[buf][0][1] + R.v[buf][1][1] + R.v[buf][2][1] + R.v[buf][3][1];
-  c = R.v[buf][0][2] + R.v[buf][1][2] + R.v[buf][2][2] + R.v[buf][3][2];
+  a = b = c = 0.0;
+  for (int w = 0; w < NW; ++w) {
+    a += R.v[buf][w][0];
+    b += R.v[buf][w][1];
+    c += R.v[buf][w][2];
+  }
   buf ^= 1;
 }
 
-__device__ __forceinline__ void block_minmax(float &mx, float &mn, BlockRed &R, int &buf) {
+template <int NW>
+__device__ __forceinline__ void block_minmax(float &mx, float &mn, BlockRed<NW> &R, int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   mx = wave_max(mx);
   mn = wave_min(mn);
@@ -80,7 +88,7 @@ __device__ __forceinline__ void block_minmax(float &mx, float &mn, BlockRed &R, 
     R.v[buf][wv][1] = (double)mn;
   }
   __syncthreads();
-  for (int w = 0; w < 4; ++w) {
+  for (int w = 0; w < NW; ++w) {
     mx = fmaxf(mx, (float)R.v[buf][w][0]);
     mn = fminf(mn, (float)R.v[buf][w][1]);
   }
@@ -174,7 +182,8 @@ __device__ double solve_lambda(const TailStats &T, double m, float eps, int pi_m
 template <int NT, class Count>
 __device__ uint32_t radix_kth(int k, int *hist, int *sel, int (*wtot)[NT / 64], int &left,
                               Count &&count) {
-  constexpr int DPT = 256 / NT;  // digits per thread, descending with the thread index
+  // digits per thread, descending with the thread index (threads past digit 0 hold none)
+  constexpr int DPT = NT >= 256 ? 1 : 256 / NT;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   uint32_t prefix = 0, pmask = 0;
   int krem = k, buf = 0;
@@ -186,7 +195,7 @@ __device__ uint32_t radix_kth(int k, int *hist, int *sel, int (*wtot)[NT / 64], 
     int c[DPT], mine = 0;
 #pragma unroll
     for (int e = 0; e < DPT; ++e) {
-      c[e] = hist[255 - DPT * t - e];
+      c[e] = DPT * t + e < 256 ? hist[255 - DPT * t - e] : 0;
       mine += c[e];
     }
     int incl = mine;
@@ -202,7 +211,7 @@ __device__ uint32_t radix_kth(int k, int *hist, int *sel, int (*wtot)[NT / 64], 
     int before = incl - mine;
 #pragma unroll
     for (int e = 0; e < DPT; ++e) {
-      if (before < krem && krem <= before + c[e]) {  // the digit holding the krem-th largest key
+      if (c[e] > 0 && before < krem && krem <= before + c[e]) {  // the digit holding the krem-th largest key
         sel[0] = 255 - DPT * t - e;
         sel[1] = krem - before;
       }
@@ -244,9 +253,11 @@ __device__ uint32_t topk_threshold(double m, double n_tail, int *hist, int *sel,
 // ---------------------------------------------------------------------------------------------
 // evict_select: lambda, mask, stored pi and index of every retained row, count, status
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunch L) {
+template <int NT>
+__global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
+  constexpr int kSelectThreads = NT;
   extern __shared__ float s_sc[];
-  __shared__ BlockRed R;
+  __shared__ BlockRed<NT / 64> R;
   __shared__ int s_tot[2][kSelectThreads / 64];
   __shared__ unsigned long long s_tot64[2][kSelectThreads / 64];
   __shared__ int s_hist[256];
@@ -397,7 +408,7 @@ __global__ __launch_bounds__(kSelectThreads) void evict_select_kernel(EvictLaunc
              });
   const float lamf = (float)lam;
 
-  // Mask and in-order write of the retained rows' pi and positions: 1024-token blocks, ranks
+  // Mask and in-order write of the retained rows' pi and positions: blocks of 4 NT tokens, ranks
   // from per-wave ballots plus the counts of the lower waves.
   const uint64_t sd = L.seed_per_unit ? L.seed_per_unit[u] : L.seed;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -952,9 +963,13 @@ hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s) {
   else if (g4 <= 4) hipLaunchKernelGGL(evict_select_reg_kernel<4>, grid, reg, 0, s, L);
   else if (g4 <= 8) hipLaunchKernelGGL(evict_select_reg_kernel<8>, grid, reg, 0, s, L);
   else if (g4 <= 12) hipLaunchKernelGGL(evict_select_reg_kernel<12>, grid, reg, 0, s, L);
-  else {
-    const size_t lds = L.stage_rows > 0 ? (size_t)((L.stage_rows + 3) / 4) * 16 : 0;
-    hipLaunchKernelGGL(evict_select_kernel, grid, dim3(kSelectThreads), lds, s, L);
+  else if (L.stage_rows > 0) {
+    // scores staged in LDS (up to 64 KB per unit, two units per CU): eight waves per unit
+    const size_t lds = (size_t)((L.stage_rows + 3) / 4) * 16;
+    hipLaunchKernelGGL(evict_select_kernel<kSelectStagedThreads>, grid, dim3(kSelectStagedThreads),
+                       lds, s, L);
+  } else {
+    hipLaunchKernelGGL(evict_select_kernel<kSelectThreads>, grid, dim3(kSelectThreads), 0, s, L);
   }
   return hipGetLastError();
 }
