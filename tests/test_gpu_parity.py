@@ -298,6 +298,8 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([4096, 300], 9, 0.5, 256),                # 8 + 1
     ([6144] * 6, 7, 0.5, 512),                 # a candidate chunk ends on the loop's last tiles
     ([8192] * 3, 4, 0.5, 2048),                # four chunks per split, the last one likewise
+    ([6144] * 2, 2, 0.7, 64),                  # > 64 splits: split scalars combined in batches
+    ([16384] * 2, 4, 0.5, 64),                 # 128 splits: candidate blocks read from the records
 ])
 def test_attend_parity(lengths, G, budget, split):
     _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))
