@@ -20,14 +20,17 @@
 //   o = sum w v (rows < GB) and Cv = sum c v (rows GB..2GB-1) together, with V in its natural
 //   row-major layout (no transpose): each fp32 weight enters as an exact three-term bf16 sum,
 //   so every product is exact and only the fp32 sums round.
-//   Range-term candidates: every weight lane keeps its four largest g^2 |v|^2 (g^2 = (1 - pi) w^2)
-//   among its rows, plus the maxima of g^2 |v|^2 and of g^2 over what it dropped; the split's
-//   record holds those 16 candidates per head, their largest |v| and the non-candidate maxima.
+//   Range-term candidates, per 512-row chunk: weight lanes take the rows of even tiles and
+//   variance lanes (same logits) those of odd tiles; each lane keeps its four largest
+//   g^2 |v|^2 (g^2 = (1 - pi) w^2) plus the maxima of g |v| and of g over what it dropped, so
+//   a chunk holds 32 candidates per head with bounds for the rest.
 //   The running max m moves lazily (only by jumps of more than 2^8 in weight).
-// attend_finalize (one wave per (unit, query head)): log-sum-exp combine of the split records,
-//   yhat, Vhat, ln Nhat, the exact range term b (only candidates whose bound can still win are
-//   re-read; a split is rescanned only if its non-candidate bound cannot exclude a larger term)
-//   and the radius r.
+// Finalize (yhat, Vhat, ln Nhat, the exact range term b and the radius r): a unit that is one
+//   split is finalized by the same wave from LDS; a unit cut into several splits by
+//   attend_finalize (one wave per (unit, head block)), which combines the split records by
+//   log-sum-exp.  Candidates are bounded a chunk block at a time; only those whose bound can
+//   still win are re-read, and a chunk is rescanned only if its non-candidate bound cannot
+//   exclude a larger term.
 #include "ebd.h"
 #include "ebd_device.hpp"
 #include "ebd_internal.hpp"

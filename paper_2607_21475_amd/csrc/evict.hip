@@ -255,11 +255,10 @@ __device__ uint32_t topk_threshold(double m, double n_tail, int *hist, int *sel,
 // ---------------------------------------------------------------------------------------------
 template <int NT>
 __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
-  constexpr int kSelectThreads = NT;
   extern __shared__ float s_sc[];
   __shared__ BlockRed<NT / 64> R;
-  __shared__ int s_tot[2][kSelectThreads / 64];
-  __shared__ unsigned long long s_tot64[2][kSelectThreads / 64];
+  __shared__ int s_tot[2][NT / 64];
+  __shared__ unsigned long long s_tot64[2][NT / 64];
   __shared__ int s_hist[256];
   __shared__ int s_sel[2];
   int rbuf = 0;
@@ -323,13 +322,13 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
   uint32_t bad = 0;
   double n_tail = 0.0, n_pos = 0.0, s_sum = 0.0;
   float s_max = 0.0f, s_minp = INFINITY;
-  for (int64_t g0 = 0; g0 < ngroups; g0 += kSelectThreads * 4) {
+  for (int64_t g0 = 0; g0 < ngroups; g0 += NT * 4) {
     float4 raw[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) raw[q] = load_raw(g0 + kSelectThreads * q + t);
+    for (int q = 0; q < 4; ++q) raw[q] = load_raw(g0 + NT * q + t);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int64_t gi = g0 + kSelectThreads * q + t;
+      const int64_t gi = g0 + NT * q + t;
       if (gi >= ngroups) break;
       // every position is checked for bad values, protected ones included
       uint32_t b2 = 0;
@@ -370,9 +369,9 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
   uint32_t tkey = 0xffffffffu;
   int tleft = 0;
   if (topk) {
-    tkey = topk_threshold<kSelectThreads>(
+    tkey = topk_threshold<NT>(
         m, n_tail, s_hist, s_sel, s_tot, tleft, st, [&](uint32_t prefix, uint32_t pmask, int shift) {
-          for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
+          for (int64_t gi = t; gi < ngroups; gi += NT) {
             const float4 s4 = group(gi);
             const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
@@ -389,7 +388,7 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
       topk ? 0.0
            : solve_lambda(ts, m, eps, L.pi_mode, st, [&](float lf, double &dH, double &dL, double &dS) {
                float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
-               for (int64_t gi = t; gi < ngroups; gi += kSelectThreads) {
+               for (int64_t gi = t; gi < ngroups; gi += NT) {
                  const float4 s4 = group(gi);
                  const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
@@ -420,7 +419,7 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
   uint64_t csum = 0;
   int64_t eq_seen = 0;  // top-k: tail positions equal to the threshold key so far
   int64_t rank0 = 0;
-  for (int64_t g0 = 0; g0 < ngroups; g0 += kSelectThreads) {
+  for (int64_t g0 = 0; g0 < ngroups; g0 += NT) {
     const int64_t gi = g0 + t;
     float p[4] = {1.0f, 1.0f, 1.0f, 1.0f};
     bool keep[4] = {false, false, false, false};
@@ -450,7 +449,7 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
       __syncthreads();
       uint64_t wpre = 0, btot = 0;
 #pragma unroll
-      for (int w = 0; w < kSelectThreads / 64; ++w) {
+      for (int w = 0; w < NT / 64; ++w) {
         const uint64_t c = s_tot64[rbuf][w];
         wpre += w < wv ? c : 0u;
         btot += c;
@@ -478,7 +477,7 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
       __syncthreads();
       int ewpre = 0, ebtot = 0;
 #pragma unroll
-      for (int w = 0; w < kSelectThreads / 64; ++w) {
+      for (int w = 0; w < NT / 64; ++w) {
         const int c = s_tot[rbuf][w];
         ewpre += w < wv ? c : 0;
         ebtot += c;
@@ -526,7 +525,7 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
     __syncthreads();
     int wpre = 0, btot = 0;
 #pragma unroll
-    for (int w = 0; w < kSelectThreads / 64; ++w) {
+    for (int w = 0; w < NT / 64; ++w) {
       const int c = s_tot[rbuf][w];
       wpre += w < wv ? c : 0;
       btot += c;
