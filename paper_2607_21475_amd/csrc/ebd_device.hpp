@@ -35,27 +35,28 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Philox4x32-10 (Salmon et al., SC 2011).  Returns the four output words.
+// Philox4x32-10 (Salmon et al., SC 2011).  Returns the four output words.  Each round's two
+// 32x32 -> 64-bit products are taken whole (one v_mad_u64_u32 each rather than a low and a high
+// multiply).
 __device__ __forceinline__ uint4 philox4x32_10(uint4 ctr, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t lo0 = 0xD2511F53u * ctr.x;
-    const uint32_t hi0 = __umulhi(0xD2511F53u, ctr.x);
-    const uint32_t lo1 = 0xCD9E8D57u * ctr.z;
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, ctr.z);
-    ctr = make_uint4(hi1 ^ ctr.y ^ k0, lo1, hi0 ^ ctr.w ^ k1, lo0);
+    const uint64_t p0 = (uint64_t)0xD2511F53u * ctr.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * ctr.z;
+    ctr = make_uint4((uint32_t)(p1 >> 32) ^ ctr.y ^ k0, (uint32_t)p1,
+                     (uint32_t)(p0 >> 32) ^ ctr.w ^ k1, (uint32_t)p0);
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
   }
   return ctr;
 }
 
-// Exact retention test x < pi * 2^32 for a stored fp32 pi in [0, 1]:
-// pi * 2^32 is exact in fp32, and for an integer x, x < t  <=>  x < ceil(t).
+// Exact retention test x < pi * 2^32 for a stored fp32 pi in [0, 1]: pi * 2^32 is exact in
+// fp32, pi = 1 keeps every x, and below 2^32, for an integer x, x < t  <=>  x < ceil(t), which
+// fits 32 bits.
 __device__ __forceinline__ bool keep_token(uint32_t x, float pi) {
   const float t = pi * 4294967296.0f;
-  const uint64_t thr = (uint64_t)ceilf(t);
-  return (uint64_t)x < thr;
+  return t >= 4294967296.0f || x < (uint32_t)ceilf(t);
 }
 
 template <int CTRL>

@@ -37,10 +37,10 @@ __device__ __forceinline__ float clean_score(float s, uint32_t &bad) {
   return s == 0.0f ? 0.0f : s;  // -0 becomes +0 (the top-k keys are the score bits)
 }
 
+// pi of a position: 1 outside the tail, clip(lambda s, eps, 1) in it.  With lambda = +inf (no
+// eviction), lambda s is +inf for s > 0 (pi = 1) and NaN for s = 0, which fmaxf drops (pi = eps).
 __device__ __forceinline__ float token_pi(bool tail, float s, float lam, float eps) {
-  if (!tail) return 1.0f;
-  if (isinf(lam)) return s > 0.0f ? 1.0f : eps;
-  return fminf(fmaxf(lam * s, eps), 1.0f);
+  return tail ? fminf(fmaxf(lam * s, eps), 1.0f) : 1.0f;
 }
 
 // Block-wide reductions over the NW waves of evict_select.  `buf` alternates between calls so
@@ -111,9 +111,11 @@ __device__ __forceinline__ uint64_t points_below(uint64_t C, uint32_t s) {
   return C > (uint64_t)s ? ((C - (uint64_t)s - 1u) >> 32) + 1u : 0u;
 }
 
-// Integer weight of a stored pi: ceil(pi 2^32), the Poisson test's exact threshold.
+// Integer weight of a stored pi: ceil(pi 2^32), the Poisson test's exact threshold (pi 2^32 is
+// exact in fp32; below 2^32 its ceiling fits 32 bits).
 __device__ __forceinline__ uint64_t pi_weight(float pi) {
-  return (uint64_t)ceilf(pi * 4294967296.0f);
+  const float t = pi * 4294967296.0f;
+  return t >= 4294967296.0f ? (1ull << 32) : (uint64_t)(uint32_t)ceilf(t);
 }
 
 // Tail statistics of a unit: |T|, positive scores, their sum, the largest score and the smallest
@@ -129,25 +131,39 @@ struct TailStats {
 // g(lambda) = H + eps L + lambda S is piecewise linear and nondecreasing: a Newton step on the
 // current piece is exact once the piece is right, and the bracket [lo, hi] with
 // g(lo) < m <= g(hi) guards every step (bisection when a step leaves it).
-template <class Pass>
-__device__ double solve_lambda(const TailStats &T, double m, float eps, int pi_mode, uint32_t &st,
-                               Pass &&pass) {
-  if (T.n_tail == 0.0) return 0.0;
+//
+// The boundary cases (no tail, the literal lambda = m / sum s, the floor, no eviction): sets
+// lambda and the status bits and returns true; false when lambda is interior and needs the
+// iteration.
+__device__ inline bool lambda_boundary(const TailStats &T, double m, float eps, int pi_mode,
+                                       uint32_t &st, double &lam) {
+  if (T.n_tail == 0.0) {
+    lam = 0.0;
+    return true;
+  }
   if (pi_mode == 1) {
     if (m <= (double)eps * T.n_tail) st |= EBD_ST_BUDGET_FLOOR;
-    return (T.s_sum > 0.0 && m > 0.0) ? m / T.s_sum : 0.0;
+    lam = (T.s_sum > 0.0 && m > 0.0) ? m / T.s_sum : 0.0;
+    return true;
   }
   if (m <= (double)eps * T.n_tail) {
     st |= EBD_ST_BUDGET_FLOOR;
-    return 0.0;
+    lam = 0.0;
+    return true;
   }
   if (m >= T.n_pos + (double)eps * (T.n_tail - T.n_pos)) {
     st |= EBD_ST_NO_EVICTION;
-    return INFINITY;
+    lam = INFINITY;
+    return true;
   }
-  double lo = (double)eps / (double)T.s_max;
-  double hi = 1.0 / (double)T.s_minp;
-  double cur = fmin(fmax(m / T.s_sum, lo), hi);
+  return false;
+}
+
+// The iteration for an interior lambda within the bracket [lo, hi] (g(lo) < m <= g(hi)),
+// starting at cur.
+template <class Pass>
+__device__ double newton_lambda(double m, float eps, double lo, double hi, double cur,
+                                Pass &&pass) {
   double pH = -1.0, pL = -1.0, pS = -1.0;
   bool from_newton = false;
   for (int it = 0; it < 96; ++it) {
@@ -172,6 +188,16 @@ __device__ double solve_lambda(const TailStats &T, double m, float eps, int pi_m
     cur = nxt;
   }
   return cur;
+}
+
+template <class Pass>
+__device__ double solve_lambda(const TailStats &T, double m, float eps, int pi_mode, uint32_t &st,
+                               Pass &&pass) {
+  double lam;
+  if (lambda_boundary(T, m, eps, pi_mode, st, lam)) return lam;
+  const double lo = (double)eps / (double)T.s_max;
+  const double hi = 1.0 / (double)T.s_minp;
+  return newton_lambda(m, eps, lo, hi, fmin(fmax(m / T.s_sum, lo), hi), pass);
 }
 
 // Top-k threshold: the k-th largest key among the tail keys (score bits, which order like the
@@ -254,11 +280,11 @@ __device__ uint32_t topk_threshold(double m, double n_tail, int *hist, int *sel,
 // evict_select: lambda, mask, stored pi and index of every retained row, count, status
 // ---------------------------------------------------------------------------------------------
 template <int NT>
-__global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4)))
+void evict_select_kernel(EvictLaunch L) {
   extern __shared__ float s_sc[];
   __shared__ BlockRed<NT / 64> R;
   __shared__ int s_tot[2][NT / 64];
-  __shared__ unsigned long long s_tot64[2][NT / 64];
   __shared__ int s_hist[256];
   __shared__ int s_sel[2];
   int rbuf = 0;
@@ -320,7 +346,8 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
   // Pass 0: read (and stage) the scores; tail statistics; bad-score flag.  Four groups per
   // thread are loaded before any is used so their latencies overlap.
   uint32_t bad = 0;
-  double n_tail = 0.0, n_pos = 0.0, s_sum = 0.0;
+  int c_tail = 0, c_pos = 0;
+  double s_sum = 0.0;
   float s_max = 0.0f, s_minp = INFINITY;
   for (int64_t g0 = 0; g0 < ngroups; g0 += NT * 4) {
     float4 raw[4];
@@ -330,31 +357,25 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
     for (int q = 0; q < 4; ++q) {
       const int64_t gi = g0 + NT * q + t;
       if (gi >= ngroups) break;
-      // every position is checked for bad values, protected ones included
-      uint32_t b2 = 0;
-      const float4 tv = tail4(gi, raw[q], b2);
-      {
-        const float rv[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (4 * gi + j < n) clean_score(rv[j], bad);
-      }
+      // every position is checked for bad values, protected ones included (positions past the
+      // end read 0, which is not bad)
+      const float4 tv = tail4(gi, raw[q], bad);
       const float v[4] = {tv.x, tv.y, tv.z, tv.w};
+      float gsum = 0.0f;  // at most 4 terms in fp32, then the running sum in fp64
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        if (v[j] >= 0.0f) {
-          n_tail += 1.0;
-          s_sum += (double)v[j];
-          if (v[j] > 0.0f) {
-            n_pos += 1.0;
-            s_minp = fminf(s_minp, v[j]);
-          }
-          s_max = fmaxf(s_max, v[j]);
-        }
+        const bool tail = v[j] >= 0.0f, pos = v[j] > 0.0f;
+        c_tail += tail ? 1 : 0;
+        c_pos += pos ? 1 : 0;
+        gsum += tail ? v[j] : 0.0f;
+        s_minp = fminf(s_minp, pos ? v[j] : INFINITY);
+        s_max = fmaxf(s_max, v[j]);
       }
+      s_sum += (double)gsum;
       if (staged) reinterpret_cast<float4 *>(s_sc)[gi] = tv;
     }
   }
+  double n_tail = (double)c_tail, n_pos = (double)c_pos;
   block_sum3(n_tail, n_pos, s_sum, R, rbuf);
   block_minmax(s_max, s_minp, R, rbuf);
   {
@@ -384,31 +405,61 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
         });
   }
   const TailStats ts{n_tail, n_pos, s_sum, s_max, s_minp};
-  const double lam =
-      topk ? 0.0
-           : solve_lambda(ts, m, eps, L.pi_mode, st, [&](float lf, double &dH, double &dL, double &dS) {
-               float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
-               for (int64_t gi = t; gi < ngroups; gi += NT) {
-                 const float4 s4 = group(gi);
-                 const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+  const double n_slots = 4.0 * (double)ngroups;  // groups of 4 positions, the last one padded
+  // One evaluation of g's pieces at lambda = lf over the unit (LDS when staged; streamed scores
+  // with four groups per thread in flight).
+  auto newton_pass = [&](float lf, double &dH, double &dL, double &dS) {
+    // slots outside the tail hold -1: lf (-1) <= eps counts them in L, corrected below
+    float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
+    auto add = [&](float4 s4) {
+      const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-                 for (int j = 0; j < 4; ++j) {
-                   const float p = lf * sv[j];
-                   const bool in = sv[j] >= 0.0f;
-                   H += (in && p >= 1.0f) ? 1.0f : 0.0f;
-                   Lo += (in && p <= eps) ? 1.0f : 0.0f;
-                   Sm += (in && p > eps && p < 1.0f) ? sv[j] : 0.0f;
-                 }
-               }
-               dH = H;
-               dL = Lo;
-               dS = Sm;
-               block_sum3(dH, dL, dS, R, rbuf);
-             });
+      for (int j = 0; j < 4; ++j) {
+        const float p = lf * sv[j];
+        const bool hb = p >= 1.0f, lb = p <= eps;
+        H += hb ? 1.0f : 0.0f;
+        Lo += lb ? 1.0f : 0.0f;
+        Sm += (hb || lb) ? 0.0f : sv[j];
+      }
+    };
+    if (staged) {
+      for (int64_t gi = t; gi < ngroups; gi += NT) add(group(gi));
+    } else {
+      for (int64_t g0 = 0; g0 < ngroups; g0 += NT * 4) {
+        float4 raw[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) raw[q] = load_raw(g0 + NT * q + t);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t dummy = 0;
+          if (g0 + NT * q + t < ngroups) add(tail4(g0 + NT * q + t, raw[q], dummy));
+        }
+      }
+    }
+    dH = H;
+    dL = Lo;
+    dS = Sm;
+    block_sum3(dH, dL, dS, R, rbuf);
+    dL -= n_slots - n_tail;  // every visited slot of the unit is either in the tail or not
+  };
+  double lam = 0.0;
+  if (!topk && !lambda_boundary(ts, m, eps, L.pi_mode, st, lam)) {
+    const double lo0 = (double)eps / (double)s_max, hi0 = 1.0 / (double)s_minp;
+    lam = newton_lambda(m, eps, lo0, hi0, fmin(fmax(m / s_sum, lo0), hi0), newton_pass);
+  }
   const float lamf = (float)lam;
 
-  // Mask and in-order write of the retained rows' pi and positions: blocks of 4 NT tokens, ranks
-  // from per-wave ballots plus the counts of the lower waves.
+  // Mask and in-order write of the retained rows' pi and positions, Q groups of 4 tokens per
+  // thread at a time (a superblock of 4 Q NT tokens; group gi = g0 + NT q + t, so positions
+  // ascend with (q, wave, lane, j)): ranks from per-(q, j) ballots plus one exchange of the
+  // per-(q, wave) counts; the systematic design's weight prefix and the top-k design's ranks of
+  // the threshold key take one exchange more.  Streamed scores: the next superblock's groups
+  // load while this one is masked.
+  constexpr int Q = 2;
+  constexpr int NW = NT / 64;
+  __shared__ int s_rk[2][Q][NW];
+  __shared__ int s_eqx[2][Q][NW];
+  __shared__ unsigned long long s_sys[2][Q][NW];
   const uint64_t sd = L.seed_per_unit ? L.seed_per_unit[u] : L.seed;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int design = L.design;
@@ -419,130 +470,171 @@ __global__ __launch_bounds__(NT) void evict_select_kernel(EvictLaunch L) {
   uint64_t csum = 0;
   int64_t eq_seen = 0;  // top-k: tail positions equal to the threshold key so far
   int64_t rank0 = 0;
-  for (int64_t g0 = 0; g0 < ngroups; g0 += NT) {
-    const int64_t gi = g0 + t;
-    float p[4] = {1.0f, 1.0f, 1.0f, 1.0f};
-    bool keep[4] = {false, false, false, false};
-    bool inr[4] = {false, false, false, false};
-    float sv[4] = {-1.0f, -1.0f, -1.0f, -1.0f};
-    if (gi < ngroups) {
-      const float4 s4 = group(gi);
-      sv[0] = s4.x;
-      sv[1] = s4.y;
-      sv[2] = s4.z;
-      sv[3] = s4.w;
+  float4 nxt[Q];
+  if (!staged) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        inr[j] = 4 * gi + j < n;
-        if (inr[j] && !topk) p[j] = token_pi(sv[j] >= 0.0f, sv[j], lamf, eps);
+    for (int q = 0; q < Q; ++q) nxt[q] = load_raw((int64_t)NT * q + t);
+  }
+  int par = 0;
+  for (int64_t g0 = 0; g0 < ngroups; g0 += (int64_t)Q * NT, par ^= 1) {
+    float sv[Q][4], p[Q][4];
+    bool inr[Q][4], keep[Q][4];
+    {
+      float4 cur[Q];
+      if (!staged) {
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          cur[q] = nxt[q];
+          nxt[q] = load_raw(g0 + (int64_t)NT * (Q + q) + t);  // zeros past the end
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int64_t gi = g0 + (int64_t)NT * q + t;
+        uint32_t dummy = 0;
+        const float4 s4 = gi >= ngroups ? make_float4(-1.0f, -1.0f, -1.0f, -1.0f)
+                                         : (staged ? group(gi) : tail4(gi, cur[q], dummy));
+        const float v[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          sv[q][j] = v[j];
+          inr[q][j] = 4 * gi + j < n;
+          p[q][j] = (inr[q][j] && !topk) ? token_pi(v[j] >= 0.0f, v[j], lamf, eps) : 1.0f;
+          keep[q][j] = false;
+        }
       }
     }
     if (design == EBD_DESIGN_SYSTEMATIC) {
-      uint64_t a[4], tsum = 0;
+      uint64_t a[Q][4], pre[Q];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        a[j] = inr[j] ? pi_weight(p[j]) : 0u;
-        tsum += a[j];
+      for (int q = 0; q < Q; ++q) {
+        uint64_t tsum = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          a[q][j] = inr[q][j] ? pi_weight(p[q][j]) : 0u;
+          tsum += a[q][j];
+        }
+        const uint64_t incl = wave_scan_u64(tsum);
+        pre[q] = incl - tsum;
+        if (lane == 63) s_sys[par][q][wv] = incl;
       }
-      const uint64_t incl = wave_scan_u64(tsum);
-      if (lane == 63) s_tot64[rbuf][wv] = incl;
       __syncthreads();
-      uint64_t wpre = 0, btot = 0;
+      uint64_t acc = csum;
 #pragma unroll
-      for (int w = 0; w < NT / 64; ++w) {
-        const uint64_t c = s_tot64[rbuf][w];
-        wpre += w < wv ? c : 0u;
-        btot += c;
-      }
-      uint64_t C = csum + wpre + incl - tsum;
+      for (int q = 0; q < Q; ++q) {
+        uint64_t C = acc + pre[q];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint64_t Cn = C + a[j];
-        keep[j] = inr[j] && points_below(Cn, sys_start) != points_below(C, sys_start);
-        C = Cn;
+        for (int w = 0; w < NW; ++w) {
+          const uint64_t c = s_sys[par][q][w];
+          C += w < wv ? c : 0u;
+          acc += c;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint64_t Cn = C + a[q][j];
+          keep[q][j] = inr[q][j] && points_below(Cn, sys_start) != points_below(C, sys_start);
+          C = Cn;
+        }
       }
-      csum += btot;
+      csum = acc;
     } else if (topk) {
       // tail positions at the threshold key are kept in position order while tleft lasts
-      bool eq[4];
-      int ebefore = 0, etot = 0;
+      int eb[Q];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        eq[j] = inr[j] && sv[j] >= 0.0f && __float_as_uint(sv[j]) == tkey;
-        const uint64_t bal = __ballot(eq[j]);
-        ebefore += __popcll(bal & below);
-        etot += __popcll(bal);
-      }
-      if (lane == 0) s_tot[rbuf][wv] = etot;
-      __syncthreads();
-      int ewpre = 0, ebtot = 0;
+      for (int q = 0; q < Q; ++q) {
+        int ebefore = 0, etot = 0;
 #pragma unroll
-      for (int w = 0; w < NT / 64; ++w) {
-        const int c = s_tot[rbuf][w];
-        ewpre += w < wv ? c : 0;
-        ebtot += c;
-      }
-      rbuf ^= 1;
-      // rank of this thread's first equal position among the unit's equal positions: the
-      // earlier blocks, the lower waves, then the lower lanes of this wave (positions ascend
-      // with block, wave and lane; within a thread, with j)
-      int64_t er = eq_seen + ewpre + ebefore;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bool tail = sv[j] >= 0.0f;
-        bool sel = false;
-        if (inr[j] && tail) {
-          const uint32_t key = __float_as_uint(sv[j]);
-          if (key > tkey) sel = true;
-          else if (eq[j]) sel = er++ < (int64_t)tleft;
+        for (int j = 0; j < 4; ++j) {
+          const uint64_t bal = __ballot(inr[q][j] && sv[q][j] >= 0.0f &&
+                                        __float_as_uint(sv[q][j]) == tkey);
+          ebefore += __popcll(bal & below);
+          etot += __popcll(bal);
         }
-        p[j] = (!inr[j] || !tail) ? 1.0f : (sel ? 1.0f : 0.0f);
-        keep[j] = inr[j] && (!tail || sel);
+        eb[q] = ebefore;
+        if (lane == 0) s_eqx[par][q][wv] = etot;
       }
-      eq_seen += ebtot;
+      __syncthreads();
+      int64_t acc = eq_seen;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        // rank of this thread's first equal position among the unit's equal positions
+        int64_t er = acc + eb[q];
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const int c = s_eqx[par][q][w];
+          er += w < wv ? c : 0;
+          acc += c;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const bool tail = sv[q][j] >= 0.0f;
+          bool sel = false;
+          if (inr[q][j] && tail) {
+            const uint32_t key = __float_as_uint(sv[q][j]);
+            if (key > tkey) sel = true;
+            else if (key == tkey) sel = er++ < (int64_t)tleft;
+          }
+          p[q][j] = (!inr[q][j] || !tail) ? 1.0f : (sel ? 1.0f : 0.0f);
+          keep[q][j] = inr[q][j] && (!tail || sel);
+        }
+      }
+      eq_seen = acc;
     } else {
-      if (gi < ngroups) {
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int64_t gi = g0 + (int64_t)NT * q + t;
+        if (gi >= ngroups) continue;
         const uint4 x = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)u, L.epoch, kPhiloxTag),
                                       (uint32_t)sd, (uint32_t)(sd >> 32));
         const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) keep[j] = inr[j] && keep_token(xw[j], p[j]);
+        for (int j = 0; j < 4; ++j) keep[q][j] = inr[q][j] && keep_token(xw[j], p[q][j]);
       }
     }
     if (L.pi_full) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (inr[j]) L.pi_full[base + 4 * gi + j] = p[j];
-    }
-    int before = 0, wtot = 0;
+      for (int q = 0; q < Q; ++q) {
+        const int64_t gi = g0 + (int64_t)NT * q + t;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint64_t bal = __ballot(keep[j]);
-      before += __popcll(bal & below);
-      wtot += __popcll(bal);
-    }
-    if (lane == 0) s_tot[rbuf][wv] = wtot;
-    __syncthreads();
-    int wpre = 0, btot = 0;
-#pragma unroll
-    for (int w = 0; w < NT / 64; ++w) {
-      const int c = s_tot[rbuf][w];
-      wpre += w < wv ? c : 0;
-      btot += c;
-    }
-    rbuf ^= 1;
-    int64_t r = rank0 + wpre + before;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (keep[j]) {
-        if (r < cap) {
-          L.pic[cbase + r] = p[j];
-          L.idxc[cbase + r] = (int32_t)(4 * gi + j);
-        }
-        ++r;
+        for (int j = 0; j < 4; ++j)
+          if (inr[q][j]) L.pi_full[base + 4 * gi + j] = p[q][j];
       }
     }
-    rank0 += btot;
+    int before[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      int b = 0, wtot = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint64_t bal = __ballot(keep[q][j]);
+        b += __popcll(bal & below);
+        wtot += __popcll(bal);
+      }
+      before[q] = b;
+      if (lane == 0) s_rk[par][q][wv] = wtot;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int64_t gi = g0 + (int64_t)NT * q + t;
+      int64_t r = rank0 + before[q];
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const int c = s_rk[par][q][w];
+        r += w < wv ? c : 0;
+        rank0 += c;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (keep[q][j]) {
+          if (r < cap) {
+            L.pic[cbase + r] = p[q][j];
+            L.idxc[cbase + r] = (int32_t)(4 * gi + j);
+          }
+          ++r;
+        }
+      }
+    }
   }
   if (t == 0) {
     if (rank0 > cap) st |= EBD_ST_CAP_OVERFLOW;
