@@ -319,7 +319,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     const int h = lane >> 3, j = lane & 7;
     float yy = 0.0f, ycv = 0.0f;
     if (h < GB) {
-      const float l = F.hs[h * kHs + kHsL];
+      const float il = 1.0f / F.hs[h * kHs + kHsL];
       float4 *oh = reinterpret_cast<float4 *>(F.o + h * kHeadDim + 16 * j);
       const float4 *cv = reinterpret_cast<const float4 *>(F.o + (GB + h) * kHeadDim + 16 * j);
       float4 *yo = reinterpret_cast<float4 *>(L.y + (uh0 + h) * kHeadDim + 16 * j);
@@ -327,10 +327,10 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       for (int q = 0; q < 4; ++q) {
         float4 a = oh[q];
         const float4 b = cv[q];
-        a.x /= l;
-        a.y /= l;
-        a.z /= l;
-        a.w /= l;
+        a.x *= il;
+        a.y *= il;
+        a.z *= il;
+        a.w *= il;
         yy += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
         ycv += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
         oh[q] = a;
@@ -376,49 +376,40 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     ub = fg * (blk[kChVmax] + hs[kHsYn]);
     return true;
   };
-  // A chunk block x = (s nchunk + k) GB + h bounds all its candidates at once: candidate j's
-  // bound is g_j F_x with F_x = f (Vmax + |yhat|) / l, so the block's largest g decides.  One
-  // lane per block; per head, the largest bound (and its candidate) goes to F.best.
+  // Chunk block x = (s nchunk + k) GB + h (16-byte aligned), or null for a chunk that is absent.
   const int nx = nsp * L.nchunk * GB;
-  auto block_bound = [&](int x, int &h, int &jmax) -> float {  // 0 for a chunk that is absent
+  auto block_at = [&](int x, int &h) -> const float * {
     h = x % GB;
-    const int sk = x / GB, s = sk / L.nchunk, k = sk % L.nchunk;
-    jmax = 0;
-    if (k * kChunkRows >= min(cnt - s * R, R)) return 0.0f;
-    const float *blk = C.base + s * C.sstride + k * C.kstride + h * C.hstride;
-    float gmax = 0.0f;
-#pragma unroll 8
-    for (int j = 0; j < kCand; ++j) {
-      const float gj = blk[kChG + j];
-      if (gj > gmax) {
-        gmax = gj;
-        jmax = j;
-      }
-    }
-    const float *hs = F.hs + h * kHs;
-    return scale_of(blk[kChM], hs[kHsM]) * gmax / hs[kHsL] * (blk[kChVmax] + hs[kHsYn]);
+    const int sk = x / GB, s = sk / L.nchunk, k = sk - s * L.nchunk;
+    if (x >= nx || k * kChunkRows >= min(cnt - s * R, R)) return nullptr;
+    return C.base + s * C.sstride + k * C.kstride + h * C.hstride;
   };
-  {
-    unsigned long long key[GB];
+  // One lane per block: candidate j's bound is g_j F with F = f (Vmax + |yhat|) / l, so the
+  // block's largest g decides; per head, the largest bound (and its candidate) goes to F.best.
+  for (int x0 = 0; x0 < nx; x0 += 64) {
+    int h;
+    const float *blk = block_at(x0 + lane, h);
+    if (blk) {
+      const float4 *g4 = reinterpret_cast<const float4 *>(blk + kChG);
+      float gmax = 0.0f;
+      int jmax = 0;
 #pragma unroll
-    for (int h = 0; h < GB; ++h) key[h] = 0ull;
-    for (int x = lane; x < nx; x += 64) {
-      int h, j;
-      const float ub = block_bound(x, h, j);
-      const unsigned long long kk =
-          ub > 0.0f ? ((unsigned long long)__float_as_uint(ub) << 32) | (unsigned)(x * kCand + j) : 0ull;
+      for (int q = 0; q < kCand / 4; ++q) {
+        const float4 v = g4[q];
+        const float gq[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int hh = 0; hh < GB; ++hh) key[hh] = (hh == h && kk > key[hh]) ? kk : key[hh];
-    }
-#pragma unroll
-    for (int h = 0; h < GB; ++h) {
-      unsigned long long k = key[h];
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long y = __shfl_xor(k, o);
-        k = y > k ? y : k;
+        for (int t = 0; t < 4; ++t) {
+          if (gq[t] > gmax) {
+            gmax = gq[t];
+            jmax = 4 * q + t;
+          }
+        }
       }
-      if (lane == 0) F.best[h] = k;
+      const float *hs = F.hs + h * kHs;
+      const float ub = scale_of(blk[kChM], hs[kHsM]) * gmax / hs[kHsL] * (blk[kChVmax] + hs[kHsYn]);
+      if (ub > 0.0f)
+        atomicMax(&F.best[h], ((unsigned long long)__float_as_uint(ub) << 32) |
+                                  (unsigned)((x0 + lane) * kCand + jmax));
     }
   }
   __syncthreads();
@@ -456,69 +447,86 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
   __syncthreads();
 
   // (4) Every other candidate whose bound exceeds its head's best value: listed, then evaluated
-  //     one per lane (a whole value row each).
+  //     sixteen at a time (four lanes per value row).
   auto eval_list = [&](int n) {
     __syncthreads();  // the list is in LDS
-    for (int i = lane; i < n; i += 64) {
-      int h, row;
-      float fg, ub;
-      decode(F.list[i], h, row, fg, ub);
-      asm volatile("" ::: "memory");  // keep yhat in LDS rather than 128 registers
-      const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + row) * kHeadDim);
-      const float *yh = F.o + h * kHeadDim;
-      uint4 vv[16];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) vv[k] = vr[k];
+    const int t4 = lane & 3;  // four lanes per candidate, 32 dims each
+    for (int i0 = 0; i0 < n; i0 += 16) {
+      const int i = i0 + (lane >> 2);
+      int h = 0, row = 0;
+      float fg = 0.0f, ub;
+      const bool have = i < n && decode(F.list[i], h, row, fg, ub);
       float d2 = 0.0f;
+      if (have) {
+        const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + row) * kHeadDim) + 4 * t4;
+        const float *yh = F.o + h * kHeadDim + 32 * t4;
+        uint4 vv[4];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const uint32_t w4[4] = {vv[k].x, vv[k].y, vv[k].z, vv[k].w};
+        for (int k = 0; k < 4; ++k) vv[k] = vr[k];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const float a = bf16_lo(w4[t]) - yh[8 * k + 2 * t];
-          const float b = bf16_hi(w4[t]) - yh[8 * k + 2 * t + 1];
-          d2 = fmaf(a, a, d2);
-          d2 = fmaf(b, b, d2);
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t w4[4] = {vv[k].x, vv[k].y, vv[k].z, vv[k].w};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const float a = bf16_lo(w4[t]) - yh[8 * k + 2 * t];
+            const float b = bf16_hi(w4[t]) - yh[8 * k + 2 * t + 1];
+            d2 = fmaf(a, a, d2);
+            d2 = fmaf(b, b, d2);
+          }
         }
       }
-      atomicMax(reinterpret_cast<unsigned *>(F.hs + h * kHs + kHsLb), __float_as_uint(fg * sqrtf(d2)));
+      d2 += __shfl_xor(d2, 1);
+      d2 += __shfl_xor(d2, 2);
+      if (have && t4 == 0)
+        atomicMax(reinterpret_cast<unsigned *>(F.hs + h * kHs + kHsLb), __float_as_uint(fg * sqrtf(d2)));
     }
     __syncthreads();
   };
-  // Only blocks whose bound exceeds the head's best value are listed from, 32 lanes per block
-  // (with a relative margin, since the block bound rounds differently from a candidate's).
+  // One lane per block marks the candidates whose bound, with a relative margin for rounding,
+  // exceeds the head's best value; a wave scan of the counts places them in the list.
   int n = 0;
   for (int x0 = 0; x0 < nx; x0 += 64) {
-    bool liveb = false;
-    if (x0 + lane < nx) {
-      int h, j;
-      const float ub = block_bound(x0 + lane, h, j);
-      liveb = ub * 1.0001f > F.hs[h * kHs + kHsLb];
+    const int x = x0 + lane;
+    int h;
+    const float *blk = block_at(x, h);
+    uint32_t bits = 0;
+    if (blk) {
+      const float *hs = F.hs + h * kHs;
+      // candidate j is listed iff f g_j (Vmax + |yhat|) / l, with a margin, exceeds the best value
+      const float thr = hs[kHsLb] / (scale_of(blk[kChM], hs[kHsM]) / hs[kHsL] *
+                                     (blk[kChVmax] + hs[kHsYn]) * 1.0002f);
+      const float4 *g4 = reinterpret_cast<const float4 *>(blk + kChG);
+#pragma unroll
+      for (int q = 0; q < kCand / 4; ++q) {
+        const float4 v = g4[q];
+        bits |= (v.x > thr ? 1u : 0u) << (4 * q);
+        bits |= (v.y > thr ? 1u : 0u) << (4 * q + 1);
+        bits |= (v.z > thr ? 1u : 0u) << (4 * q + 2);
+        bits |= (v.w > thr ? 1u : 0u) << (4 * q + 3);
+      }
+      const unsigned long long bk = F.best[h];  // evaluated in step (3)
+      const unsigned jb = (unsigned)(bk & 0xffffffffull) - (unsigned)(x * kCand);
+      if (bk && jb < (unsigned)kCand) bits &= ~(1u << jb);
     }
-    uint64_t mb = __ballot(liveb);
-    while (mb) {
-      const int xa = x0 + (int)__builtin_ctzll(mb);
-      mb &= mb - 1;
-      int xb = -1;
-      if (mb) {
-        xb = x0 + (int)__builtin_ctzll(mb);
-        mb &= mb - 1;
-      }
-      const int xx = lane < 32 ? xa : xb;
-      const int e = xx * kCand + (lane & 31);
-      int h = 0, row;
-      float fg, ub;
-      bool live = false;
-      if (xx >= 0 && decode(e, h, row, fg, ub))
-        live = ub > F.hs[h * kHs + kHsLb] && (unsigned)e != (unsigned)(F.best[h] & 0xffffffffull);
-      const uint64_t m = __ballot(live);
-      if (live) {
-        const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-        F.list[n + rank] = e;
-      }
-      n += (int)__popcll(m);
-      if (n > kListCap - 64) {
+    // exclusive prefix of the counts by bit planes (counts are at most kCand = 32)
+    const int mine = __popc(bits);
+    int excl = 0, total = 0;
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+      const uint64_t m = __ballot((mine >> b) & 1);
+      excl += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) << b;
+      total += (int)__popcll(m) << b;
+    }
+    // entries p of this group (p = excl .. excl + mine - 1 for this lane) go out in list-sized
+    // windows
+    for (int done = 0; done < total;) {
+      const int take = min(kListCap - n, total - done);
+      int p = excl;
+      for (uint32_t m = bits; m; m &= m - 1, ++p)
+        if (p >= done && p < done + take) F.list[n + p - done] = x * kCand + __builtin_ctz(m);
+      n += take;
+      done += take;
+      if (n == kListCap) {
         eval_list(n);
         n = 0;
       }
