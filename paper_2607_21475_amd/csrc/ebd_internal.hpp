@@ -9,8 +9,7 @@ namespace ebd {
 
 constexpr int kHeadDim = 128;                // rows of K, V and q are 128 bf16
 constexpr int kEvictStageMax = 16384;        // scores staged in LDS (64 KB) up to this length
-constexpr int kSelectThreads = 256;          // evict_select, scores streamed: four waves per unit
-constexpr int kSelectStagedThreads = 512;    // evict_select, scores in LDS: eight waves per unit
+constexpr int kSelectThreads = 512;          // evict_select (scores in LDS or streamed): eight waves per unit
 constexpr int kSelectRegThreads = 128;       // evict_select_reg: two waves per unit, <= 6144 tokens
 constexpr int kCopyThreads = 256;            // evict_copy: 16 lanes per 256-byte row
 constexpr int kCopyRows = 128;               // retained rows per evict_copy work-group

@@ -5,8 +5,8 @@
 //   evict_select_reg (units of at most 6144 tokens) one work-group of 2 waves per unit, the scores
 //                 in registers, so that every unit of a large batch is resident at once; the same
 //                 steps as evict_select below with one barrier per reduction or prefix.
-//   evict_select  (longer units) one work-group per unit (8 waves while the scores are staged in
-//                 LDS, 4 when they are streamed).  Stages the unit's scores in LDS (up to
+//   evict_select  (longer units) one work-group of 8 waves per unit, two per CU.  Stages the
+//                 unit's scores in LDS (up to
 //                 16384 tokens, protected positions marked by a negative sentinel; longer units
 //                 are re-read from memory), solves lambda with sum_T clip(lambda s, eps, 1) = m by
 //                 safeguarded Newton steps on the piecewise linear g(lambda) (exact once the
@@ -1054,13 +1054,11 @@ hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s) {
   else if (g4 <= 4) hipLaunchKernelGGL(evict_select_reg_kernel<4>, grid, reg, 0, s, L);
   else if (g4 <= 8) hipLaunchKernelGGL(evict_select_reg_kernel<8>, grid, reg, 0, s, L);
   else if (g4 <= 12) hipLaunchKernelGGL(evict_select_reg_kernel<12>, grid, reg, 0, s, L);
-  else if (L.stage_rows > 0) {
-    // scores staged in LDS (up to 64 KB per unit, two units per CU): eight waves per unit
+  else {
+    // eight waves per unit, two units per CU: scores staged in LDS (up to 64 KB per unit) or,
+    // for longer units, streamed from memory on every pass
     const size_t lds = (size_t)((L.stage_rows + 3) / 4) * 16;
-    hipLaunchKernelGGL(evict_select_kernel<kSelectStagedThreads>, grid, dim3(kSelectStagedThreads),
-                       lds, s, L);
-  } else {
-    hipLaunchKernelGGL(evict_select_kernel<kSelectThreads>, grid, dim3(kSelectThreads), 0, s, L);
+    hipLaunchKernelGGL(evict_select_kernel<kSelectThreads>, grid, dim3(kSelectThreads), lds, s, L);
   }
   return hipGetLastError();
 }
