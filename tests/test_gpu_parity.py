@@ -378,6 +378,29 @@ def test_attend_range_term_rescan_path():
     _check_attend(out, res, q, G)
 
 
+def test_attend_range_term_long_candidate_list():
+    """Equal norms and weights in one long split: every candidate's bound beats the best value, so
+    the finalize lists far more candidates than one evaluation batch holds (several batches)."""
+    _say("attend long candidate list")
+    from paper_2607_21475_amd import cache
+
+    U, n, G = 2, 16384, 2
+    lengths = [n] * U
+    K = torch.zeros((U * n, 128), dtype=torch.bfloat16, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    sign = torch.randint(0, 2, (U * n, 128), generator=g, device="cuda").float() * 2 - 1
+    V = sign.to(torch.bfloat16)
+    seq_off = synth.seq_offsets(lengths, "cuda")
+    sc = torch.ones(U * n, dtype=torch.float32, device="cuda")
+    q = synth.make_queries(U, G, seed=6, device="cuda")
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.45, seed=9)
+    assert 4096 < int(_np(out.count).min()) and int(_np(out.count).max()) <= 8192
+    res = cache.attend_certify(out, q, split_rows=8192)  # one split per unit: the fused finalize
+    torch.cuda.synchronize()
+    _check_attend(out, res, q, G)
+
+
 def test_attend_pi_one_is_full_attention():
     """Budget 1: nothing evicted, pi = 1 everywhere, so yhat is full attention and Vhat = b = r = 0."""
     _say("attend pi=1")
