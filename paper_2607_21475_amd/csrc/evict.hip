@@ -78,6 +78,27 @@ __device__ __forceinline__ void block_sum3(double &a, double &b, double &c, Bloc
   buf ^= 1;
 }
 
+// As block_sum3 for a and b that are already wave totals (the same in every lane).
+template <int NW>
+__device__ __forceinline__ void block_sum_wave2(double &a, double &b, double &c, BlockRed<NW> &R,
+                                                int &buf) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  c = wave_sum_d(c);
+  if (lane == 0) {
+    R.v[buf][wv][0] = a;
+    R.v[buf][wv][1] = b;
+    R.v[buf][wv][2] = c;
+  }
+  __syncthreads();
+  a = b = c = 0.0;
+  for (int w = 0; w < NW; ++w) {
+    a += R.v[buf][w][0];
+    b += R.v[buf][w][1];
+    c += R.v[buf][w][2];
+  }
+  buf ^= 1;
+}
+
 template <int NW>
 __device__ __forceinline__ void block_minmax(float &mx, float &mn, BlockRed<NW> &R, int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -405,42 +426,49 @@ void evict_select_kernel(EvictLaunch L) {
         });
   }
   const TailStats ts{n_tail, n_pos, s_sum, s_max, s_minp};
-  const double n_slots = 4.0 * (double)ngroups;  // groups of 4 positions, the last one padded
   // One evaluation of g's pieces at lambda = lf over the unit (LDS when staged; streamed scores
-  // with four groups per thread in flight).
+  // with four groups per thread in flight).  The loops are uniform over the work-group, so the
+  // counts are wave ballots; slots past the unit read -1 like every slot outside the tail.
   auto newton_pass = [&](float lf, double &dH, double &dL, double &dS) {
-    // slots outside the tail hold -1: lf (-1) <= eps counts them in L, corrected below
-    float H = 0.0f, Lo = 0.0f, Sm = 0.0f;
+    int H = 0, Lo = 0;  // wave totals
+    float Sm = 0.0f;
     auto add = [&](float4 s4) {
       const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float p = lf * sv[j];
         const bool hb = p >= 1.0f, lb = p <= eps;
-        H += hb ? 1.0f : 0.0f;
-        Lo += lb ? 1.0f : 0.0f;
+        H += __popcll(__ballot(hb));
+        Lo += __popcll(__ballot(lb));
         Sm += (hb || lb) ? 0.0f : sv[j];
       }
+      asm volatile("" : "+s"(H), "+s"(Lo));  // counted now: no lane masks held across groups
     };
+    const float4 none = make_float4(-1.0f, -1.0f, -1.0f, -1.0f);
+    int64_t slots = 0;  // slots visited by the work-group
     if (staged) {
-      for (int64_t gi = t; gi < ngroups; gi += NT) add(group(gi));
+      for (int64_t g0 = 0; g0 < ngroups; g0 += NT) {
+        add(g0 + t < ngroups ? group(g0 + t) : none);
+        slots += 4 * NT;
+      }
     } else {
       for (int64_t g0 = 0; g0 < ngroups; g0 += NT * 4) {
         float4 raw[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) raw[q] = load_raw(g0 + NT * q + t);
+        for (int q = 0; q < 4; ++q) raw[q] = load_raw(g0 + NT * q + t);  // 0 past the end
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           uint32_t dummy = 0;
-          if (g0 + NT * q + t < ngroups) add(tail4(g0 + NT * q + t, raw[q], dummy));
+          add(tail4(g0 + NT * q + t, raw[q], dummy));  // -1 past the end
         }
+        slots += 16 * NT;
       }
     }
-    dH = H;
-    dL = Lo;
+    dH = (double)H;
+    dL = (double)Lo;
     dS = Sm;
-    block_sum3(dH, dL, dS, R, rbuf);
-    dL -= n_slots - n_tail;  // every visited slot of the unit is either in the tail or not
+    block_sum_wave2(dH, dL, dS, R, rbuf);
+    dL -= (double)slots - n_tail;  // every visited slot is either in the tail or not
   };
   double lam = 0.0;
   if (!topk && !lambda_boundary(ts, m, eps, L.pi_mode, st, lam)) {
@@ -759,6 +787,7 @@ void evict_select_reg_kernel(EvictLaunch L) {
         s_max = fmaxf(s_max, tail ? c : 0.0f);
         s_minp = fminf(s_minp, (tail && c > 0.0f) ? c : INFINITY);
       }
+      asm volatile("" : "+s"(n_bad), "+s"(n_tail), "+s"(n_pos));  // counted now, masks dropped
       __builtin_amdgcn_sched_barrier(0);  // one group at a time: bounded register pressure
     }
   }
@@ -815,7 +844,7 @@ void evict_select_reg_kernel(EvictLaunch L) {
                int H = 0, Lo = 0;  // wave totals (ballots)
                float Sm = 0.0f;
 #pragma unroll
-               for (int q = 0; q < G4; ++q)
+               for (int q = 0; q < G4; ++q) {
 #pragma unroll
                  for (int j = 0; j < 4; ++j) {
                    const float p = lf * sv[q][j];
@@ -824,6 +853,10 @@ void evict_select_reg_kernel(EvictLaunch L) {
                    Lo += __popcll(__ballot(lb));
                    Sm += (hb || lb) ? 0.0f : sv[q][j];
                  }
+                 // counted per group: the compiler would otherwise keep 2 x 4 G4 lane masks until
+                 // the one lane that publishes the totals
+                 asm volatile("" : "+s"(H), "+s"(Lo));
+               }
                bsum(H, Lo, Sm, dH, dL, dS);
                dL -= n_out;
              });
