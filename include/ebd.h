@@ -139,6 +139,8 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
  *   (0 means 1e-9): the confidence level and normaliser of eq. (4).
  *   split_rows: retained rows per split, one wave each (0 = library choice; else a
  *   multiple of 16 in [16, 8192]).  Retained rows of a unit beyond max_rows are ignored.
+ *   A unit spans at most 4096 splits: max_rows above 4096 split rows (with the library's
+ *   choice, above 4096 x 4096 rows) returns EBD_ERR_UNSUPPORTED.
  *   flags: 0, or EBD_F_NO_OFFSET: y and ln N are those of the uncorrected retained softmax
  *   (the logit offset -ln pi dropped, the ablation arm of Sec. 5 and App. "Experimental
  *   details"), while vhat, b and r stay the Hajek certificate of the same retained set;

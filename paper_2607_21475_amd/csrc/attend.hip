@@ -803,31 +803,20 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
 }
 
 // attend_finalize: one wave per (unit, head block) when units are cut into several splits.  The
-// split records are combined into LDS, the candidate blocks of every split copied there too when
-// they fit (kFinStageBytes), then the unit is finalized like a fused split.  Every global read of
-// the records is issued in batches, so the wave waits on a handful of round trips rather than
-// one per candidate.
-constexpr size_t kFinStageBytes = 48 * 1024;
-
-template <int GB>
-__host__ __device__ constexpr size_t fin_stage_bytes(int32_t nsplit, int32_t nchunk) {
-  return (size_t)nsplit * GB * nchunk * kChunkFloats * sizeof(float);
-}
-// Float offsets in the finalize's LDS: the split scales after FinLds, the staged blocks after
-// them on a 16-byte boundary.
+// split records are combined into LDS, then the unit is finalized like a fused split, reading
+// the candidate blocks from the records (a lane per block, whole blocks as float4).  Every global
+// read of the records is issued in batches, so the wave waits on a handful of round trips rather
+// than one per split or candidate.
+// Float offset of the split scale factors in the finalize's LDS (after FinLds).
 template <int GB>
 __host__ __device__ constexpr size_t fin_scale_off() {
   return FinLds<GB>::bytes() / sizeof(float);
-}
-template <int GB>
-__host__ __device__ constexpr size_t fin_stage_off(int32_t nsplit) {
-  return (fin_scale_off<GB>() + (size_t)nsplit * GB + 3) / 4 * 4;
 }
 
 template <int GB>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void attend_finalize_kernel(AttendLaunch L, int h0) {
-  extern __shared__ float s_fin[];  // FinLds, then the split scale factors, then staged blocks
+  extern __shared__ float s_fin[];  // FinLds, then the split scale factors
   const int u = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t cbase = L.cap_off[u];
@@ -842,9 +831,7 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
   const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h0) * L.rec;  // (s, h) at s G rec + h rec
   const int64_t sstride = (int64_t)L.G * L.rec;
   FinLds<GB> F(s_fin);
-  float *fsc = s_fin + fin_scale_off<GB>();           // [nsplit][GB]: scale of (s, h)
-  float *stage = s_fin + fin_stage_off<GB>(L.nsplit);  // [nsp][GB][nchunk][kChunkFloats]
-  const bool staged = fin_stage_bytes<GB>(L.nsplit, L.nchunk) <= kFinStageBytes;
+  float *fsc = s_fin + fin_scale_off<GB>();  // [nsplit][GB]: scale of (s, h)
 
   // Scalars (M, l, C0, C2) of every (split, head): one float4 per lane and head, all in flight.
   for (int s0 = 0; s0 < nsp; s0 += 64) {
@@ -876,15 +863,16 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
   for (int e = lane; e < nsp * GB; e += 64) fsc[e] = scale_of(fsc[e], F.hs[(e % GB) * kHs + kHsM]);
   __syncthreads();
 
-  // o and Cv: two dims per lane, every slot of two splits in flight at once.
+  // o and Cv: two dims per lane, every slot of SP splits in flight at once.
   {
+    constexpr int SP = GB <= 4 ? 4 : 2;
     float2 acc[2 * GB];
 #pragma unroll
     for (int slot = 0; slot < 2 * GB; ++slot) acc[slot] = make_float2(0.0f, 0.0f);
-    for (int sp = 0; sp < nsp; sp += 2) {
-      float2 a[2][2 * GB];
+    for (int sp = 0; sp < nsp; sp += SP) {
+      float2 a[SP][2 * GB];
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int q = 0; q < SP; ++q)
 #pragma unroll
         for (int slot = 0; slot < 2 * GB; ++slot) {
           const int h = slot < GB ? slot : slot - GB;
@@ -894,7 +882,7 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
                                     : make_float2(0.0f, 0.0f);
         }
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
+      for (int q = 0; q < SP; ++q) {
         if (sp + q >= nsp) break;
 #pragma unroll
         for (int slot = 0; slot < 2 * GB; ++slot) {
@@ -911,39 +899,14 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
       reinterpret_cast<float2 *>(F.o + slot * kHeadDim)[lane] = acc[slot];
   }
 
-  // Candidate blocks: every split's chunk blocks of these heads into LDS, 8 float4 per lane in
-  // flight (blocks of chunks a split does not have are copied too and never read).
-  const int per4 = L.nchunk * kChunkFloats / 4;  // float4 per (split, head)
-  if (staged) {
-    const int n4 = nsp * GB * per4;
-    float4 *dst = reinterpret_cast<float4 *>(stage);
-    for (int i0 = 0; i0 < n4; i0 += 8 * 64) {
-      float4 v[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int i = min(i0 + 64 * k + lane, n4 - 1);  // past the end: a valid element, unused
-        const int sh = i / per4, o = i % per4;
-        v[k] = reinterpret_cast<const float4 *>(rec0 + (sh / GB) * sstride + (sh % GB) * L.rec +
-                                                kRecChunks)[o];
-      }
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int i = i0 + 64 * k + lane;
-        if (i < n4) dst[i] = v[k];
-      }
-    }
-  }
   __syncthreads();
-  const CandSrc C = staged ? CandSrc{stage, (int64_t)GB * per4 * 4, kChunkFloats, per4 * 4}
-                           : CandSrc{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
+  const CandSrc C{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
   finalize_block<GB>(L, u, h0, cnt, cbase, nsp, C, F);
 }
 
 template <int GB>
 size_t attend_finalize_lds(const AttendLaunch &L) {
-  const size_t b = fin_stage_off<GB>(L.nsplit) * sizeof(float);
-  const size_t st = fin_stage_bytes<GB>(L.nsplit, L.nchunk);
-  return st <= kFinStageBytes ? b + st : b;
+  return (fin_scale_off<GB>() + (size_t)L.nsplit * GB) * sizeof(float);
 }
 
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows) {

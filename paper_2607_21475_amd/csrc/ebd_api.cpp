@@ -269,6 +269,7 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
     return EBD_ERR_INVALID_ARG;
   const int32_t sr = attend_split_rows(p);
   const int32_t nsplit = attend_nsplit(p, sr);
+  if (nsplit > kMaxSplits) return EBD_ERR_UNSUPPORTED;
   const size_t need = attend_workspace_bytes(p->num_units, nsplit, p->group, sr);
   if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
   const ebd_status ds = check_device();

@@ -73,25 +73,70 @@ __device__ __forceinline__ float row16_sum(float x) {
   return x;
 }
 
+// Wave reductions: DPP within each 16-lane row (every lane of a row gets the row's result), then
+// the four row results by lane reads, so the result is the same in every lane and the order of
+// the operations is fixed.  Every lane of the wave must be active.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+template <class T>
+struct LaneBits;
+template <>
+struct LaneBits<float> {
+  template <int CTRL>
+  __device__ static float dpp(float x) { return __int_as_float(dpp_i<CTRL>(__float_as_int(x))); }
+  __device__ static float read(float x, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+  }
+};
+template <>
+struct LaneBits<int> {
+  template <int CTRL>
+  __device__ static int dpp(int x) { return dpp_i<CTRL>(x); }
+  __device__ static int read(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
+};
+template <>
+struct LaneBits<double> {
+  template <int CTRL>
+  __device__ static double dpp(double x) {
+    const unsigned long long b = (unsigned long long)__double_as_longlong(x);
+    const unsigned lo = (unsigned)dpp_i<CTRL>((int)(unsigned)b);
+    const unsigned hi = (unsigned)dpp_i<CTRL>((int)(unsigned)(b >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+  }
+  __device__ static double read(double x, int l) {
+    const unsigned long long b = (unsigned long long)__double_as_longlong(x);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+  }
+};
+
+template <class T, class Op>
+__device__ __forceinline__ T wave_reduce(T x, Op op) {
+  using B = LaneBits<T>;
+  x = op(x, B::template dpp<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = op(x, B::template dpp<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = op(x, B::template dpp<0x141>(x));  // row_half_mirror
+  x = op(x, B::template dpp<0x140>(x));  // row_mirror
+  return op(op(B::read(x, 0), B::read(x, 16)), op(B::read(x, 32), B::read(x, 48)));
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
+  return wave_reduce(x, [](float a, float b) { return a + b; });
 }
 __device__ __forceinline__ double wave_sum(double x) {
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
+  return wave_reduce(x, [](double a, double b) { return a + b; });
 }
 __device__ __forceinline__ int wave_sum(int x) {
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
+  return wave_reduce(x, [](int a, int b) { return a + b; });
 }
 __device__ __forceinline__ float wave_max(float x) {
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
+  return wave_reduce(x, [](float a, float b) { return fmaxf(a, b); });
 }
 __device__ __forceinline__ float wave_min(float x) {
-  for (int o = 32; o > 0; o >>= 1) x = fminf(x, __shfl_xor(x, o));
-  return x;
+  return wave_reduce(x, [](float a, float b) { return fminf(a, b); });
 }
 
 }  // namespace ebd

@@ -20,6 +20,7 @@ constexpr int kSplitMaxRows = 4096;  // default split length cap (bounds the lau
 constexpr int kSplitMinRows = 256;   // default split length floor
 constexpr int kSplitWaves = 1536;    // default: cut units until the launch has this many waves
 constexpr int kSplitRowsLimit = 8192;  // largest split a caller may ask for (LDS of one wave)
+constexpr int kMaxSplits = 4096;       // splits per unit (the finalize keeps a scale per split and head in LDS)
 constexpr size_t kSplitLdsBudget = 20480;  // LDS of one split wave at two waves per SIMD (160 KB / 8)
 constexpr int kScoresMaxQueries = 64;  // queries per ebd_scores call (four MFMA blocks)
 constexpr int kChunkRows = 512;      // range-term candidates are kept per chunk of a split

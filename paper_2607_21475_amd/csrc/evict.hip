@@ -50,19 +50,16 @@ struct BlockRed {
   double v[2][NW][4];
 };
 
-__device__ __forceinline__ double wave_sum_d(double x) {
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
-}
+
 
 // Sums a, b, c (each exact in double for counts) over the block; all threads get the totals.
 template <int NW>
 __device__ __forceinline__ void block_sum3(double &a, double &b, double &c, BlockRed<NW> &R,
                                            int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  a = wave_sum_d(a);
-  b = wave_sum_d(b);
-  c = wave_sum_d(c);
+  a = wave_sum(a);
+  b = wave_sum(b);
+  c = wave_sum(c);
   if (lane == 0) {
     R.v[buf][wv][0] = a;
     R.v[buf][wv][1] = b;
@@ -83,7 +80,7 @@ template <int NW>
 __device__ __forceinline__ void block_sum_wave2(double &a, double &b, double &c, BlockRed<NW> &R,
                                                 int &buf) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  c = wave_sum_d(c);
+  c = wave_sum(c);
   if (lane == 0) {
     R.v[buf][wv][0] = a;
     R.v[buf][wv][1] = b;

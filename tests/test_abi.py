@@ -120,6 +120,9 @@ def test_attend_argument_validation():
     assert call(params(delta=1.0)) == ebd.EBD_ERR_INVALID_ARG
     assert call(params(), ws_bytes=100) == ebd.EBD_ERR_WORKSPACE
     assert call(params(U=0)) == ebd.EBD_OK
+    # at most 4096 splits per unit
+    assert call(params(split=16, max_rows=16 * 4097)) == ebd.EBD_ERR_UNSUPPORTED
+    assert call(params(split=16, max_rows=16 * 4096), ws_bytes=100) == ebd.EBD_ERR_WORKSPACE
 
 
 def test_workspace_sizes():
