@@ -177,8 +177,22 @@ __device__ inline bool lambda_boundary(const TailStats &T, double m, float eps, 
   return false;
 }
 
+// Where the scores of the evaluated piece lie: the smallest score of H, the largest and smallest
+// of the middle, the largest tail score of L.  A lambda whose fp32 products keep every token on
+// its side (monotone in s) gives a pass with exactly the same counts and sum.
+struct PieceEdges {
+  bool valid;  // false: not tracked by this pass
+  float h_min, m_max, m_min, l_max;
+  __device__ bool keeps(float lf, float eps) const {
+    return valid && lf * h_min >= 1.0f && lf * m_max < 1.0f && lf * m_min > eps &&
+           lf * l_max <= eps;
+  }
+};
+
 // The iteration for an interior lambda within the bracket [lo, hi] (g(lo) < m <= g(hi)),
-// starting at cur.
+// starting at cur.  pass(lf, H, L, S, edges) evaluates the piece at lf.  A Newton step that
+// stays on the evaluated piece is final: the next pass would find the same piece and stop there,
+// so a pass that reports the piece's edges saves that confirming pass.
 template <class Pass>
 __device__ double newton_lambda(double m, float eps, double lo, double hi, double cur,
                                 Pass &&pass) {
@@ -187,7 +201,8 @@ __device__ double newton_lambda(double m, float eps, double lo, double hi, doubl
   for (int it = 0; it < 96; ++it) {
     const float lf = (float)cur;
     double dH, dL, dS;
-    pass(lf, dH, dL, dS);
+    PieceEdges e;
+    pass(lf, dH, dL, dS, e);
     if (from_newton && dH == pH && dL == pL && dS == pS) break;  // same piece: cur is exact
     const double g = dH + (double)eps * dL + (double)lf * dS;
     if (g < m) lo = (double)lf;
@@ -198,6 +213,10 @@ __device__ double newton_lambda(double m, float eps, double lo, double hi, doubl
     if (!from_newton) nxt = 0.5 * (lo + hi);
     if ((float)nxt == lf || hi - lo <= 1e-9 * hi) {
       cur = from_newton ? nxt : cur;
+      break;
+    }
+    if (from_newton && e.keeps((float)nxt, eps)) {
+      cur = nxt;
       break;
     }
     pH = dH;
@@ -302,6 +321,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4)))
 void evict_select_kernel(EvictLaunch L) {
   extern __shared__ float s_sc[];
   __shared__ BlockRed<NT / 64> R;
+  __shared__ float4 s_edge[2][NT / 64];  // per wave: the edges of a streamed Newton pass
   __shared__ int s_tot[2][NT / 64];
   __shared__ int s_hist[256];
   __shared__ int s_sel[2];
@@ -425,11 +445,14 @@ void evict_select_kernel(EvictLaunch L) {
   const TailStats ts{n_tail, n_pos, s_sum, s_max, s_minp};
   // One evaluation of g's pieces at lambda = lf over the unit (LDS when staged; streamed scores
   // with four groups per thread in flight).  The loops are uniform over the work-group, so the
-  // counts are wave ballots; slots past the unit read -1 like every slot outside the tail.
-  auto newton_pass = [&](float lf, double &dH, double &dL, double &dS) {
+  // counts are wave ballots; slots past the unit read -1 like every slot outside the tail.  A
+  // streamed pass, whose cost is the re-read of the scores, also reports the piece's edges so
+  // that the solve can skip its confirming pass.
+  auto newton_pass = [&](float lf, double &dH, double &dL, double &dS, PieceEdges &edges) {
     int H = 0, Lo = 0;  // wave totals
     float Sm = 0.0f;
-    auto add = [&](float4 s4) {
+    float h_min = INFINITY, m_max = 0.0f, m_min = INFINITY, l_max = 0.0f;
+    auto add = [&](float4 s4, bool track) {
       const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -437,7 +460,14 @@ void evict_select_kernel(EvictLaunch L) {
         const bool hb = p >= 1.0f, lb = p <= eps;
         H += __popcll(__ballot(hb));
         Lo += __popcll(__ballot(lb));
-        Sm += (hb || lb) ? 0.0f : sv[j];
+        const float mid = (hb || lb) ? 0.0f : sv[j];
+        Sm += mid;
+        if (track) {
+          h_min = fminf(h_min, hb ? sv[j] : INFINITY);
+          m_max = fmaxf(m_max, mid);
+          m_min = fminf(m_min, (hb || lb) ? INFINITY : sv[j]);
+          l_max = fmaxf(l_max, lb ? sv[j] : 0.0f);
+        }
       }
       asm volatile("" : "+s"(H), "+s"(Lo));  // counted now: no lane masks held across groups
     };
@@ -445,7 +475,7 @@ void evict_select_kernel(EvictLaunch L) {
     int64_t slots = 0;  // slots visited by the work-group
     if (staged) {
       for (int64_t g0 = 0; g0 < ngroups; g0 += NT) {
-        add(g0 + t < ngroups ? group(g0 + t) : none);
+        add(g0 + t < ngroups ? group(g0 + t) : none, false);
         slots += 4 * NT;
       }
     } else {
@@ -456,16 +486,37 @@ void evict_select_kernel(EvictLaunch L) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           uint32_t dummy = 0;
-          add(tail4(g0 + NT * q + t, raw[q], dummy));  // -1 past the end
+          add(tail4(g0 + NT * q + t, raw[q], dummy), true);  // -1 past the end
         }
         slots += 16 * NT;
       }
     }
+    edges.valid = !staged;
+    if (!staged) {  // the edges over the work-group, published by the barrier of the sums below
+      h_min = wave_min(h_min);
+      m_max = wave_max(m_max);
+      m_min = wave_min(m_min);
+      l_max = wave_max(l_max);
+      if (lane == 0) s_edge[rbuf][wv] = make_float4(h_min, m_max, m_min, l_max);
+    }
+    const int eb = rbuf;
     dH = (double)H;
     dL = (double)Lo;
     dS = Sm;
     block_sum_wave2(dH, dL, dS, R, rbuf);
     dL -= (double)slots - n_tail;  // every visited slot is either in the tail or not
+    if (!staged) {
+      edges.h_min = edges.m_min = INFINITY;
+      edges.m_max = edges.l_max = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NT / 64; ++w) {
+        const float4 e4 = s_edge[eb][w];
+        edges.h_min = fminf(edges.h_min, e4.x);
+        edges.m_max = fmaxf(edges.m_max, e4.y);
+        edges.m_min = fminf(edges.m_min, e4.z);
+        edges.l_max = fmaxf(edges.l_max, e4.w);
+      }
+    }
   };
   double lam = 0.0;
   if (!topk && !lambda_boundary(ts, m, eps, L.pi_mode, st, lam)) {
@@ -837,7 +888,9 @@ void evict_select_reg_kernel(EvictLaunch L) {
   const TailStats ts{d_tail, d_pos, d_sum, s_max, s_minp};
   const double lam =
       topk ? 0.0
-           : solve_lambda(ts, m, eps, L.pi_mode, st, [&](float lf, double &dH, double &dL, double &dS) {
+           : solve_lambda(ts, m, eps, L.pi_mode, st, [&](float lf, double &dH, double &dL, double &dS,
+                                                          PieceEdges &edges) {
+               edges.valid = false;
                int H = 0, Lo = 0;  // wave totals (ballots)
                float Sm = 0.0f;
 #pragma unroll
