@@ -144,7 +144,7 @@ struct TailStats {
 };
 
 // lambda of eq. (2) with sum_T clip(lambda s, eps, 1) = m, plus the status bits of the boundary
-// cases.  `pass(lf, H, L, S)` gives the unit's totals at lambda = lf: tail positions with
+// cases.  `pass(lf, H, L, S, edges)` gives the unit's totals at lambda = lf: tail positions with
 // lf s >= 1 (H), with lf s <= eps (L), and the sum of the scores in between (S).
 // g(lambda) = H + eps L + lambda S is piecewise linear and nondecreasing: a Newton step on the
 // current piece is exact once the piece is right, and the bracket [lo, hi] with
