@@ -122,6 +122,23 @@ def test_evict_pareto_scores_and_floor_0005():
     _check_evict(lengths, K, V, seq_off, sc, out, budget=0.1, pi_min=0.005, seed=2, epoch=3)
 
 
+def test_evict_streamed_pareto_lambda():
+    """Units longer than the LDS stage with heavy-tailed scores and the 0.005 floor (many scores
+    clip at 1 and at the floor): the streamed sampler's lambda against the oracle's fp64 solve,
+    and the full parity check."""
+    lengths = [40000, 70001, 131072]
+    _say("evict streamed pareto lambda")
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=8, scores="pareto")
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.1, pi_min=0.005, seed=4)
+    _check_evict(lengths, K, V, seq_off, sc, out, budget=0.1, pi_min=0.005, seed=4)
+    off = _np(seq_off)
+    s = _np(sc)
+    lam_gpu = _np(out.lam)
+    for u in range(len(lengths)):
+        _, lam, _ = oracle.inclusion_probs(s[off[u]:off[u + 1]], 4, 64, 0.1, 0.005)
+        assert abs(float(lam_gpu[u]) - lam) <= 1e-6 * lam, (u, float(lam_gpu[u]), lam)
+
+
 def test_evict_literal_mode_and_protection():
     lengths = [3000, 500, 64]
     _say("evict literal mode")
