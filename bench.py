@@ -243,6 +243,8 @@ def main() -> int:
         # y, vhat, lse, b, r per query head of budgets whose units span several splits
         "attend_finalize": (nb - nfused) * U * G * (512 + 16),
     }
+    if kt["evict_copy"][1] == 0:  # units past the register sampler: evict_select gathers the rows
+        alg["evict_select"] += alg["evict_copy"]
     kern = {}
     for k in KERNELS:
         ms, launches = kt[k]

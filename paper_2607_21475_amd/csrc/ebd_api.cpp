@@ -250,7 +250,7 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (timed("evict_select", s, [&] { return launch_evict_select(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
-  if (L.copy_blocks > 0 &&
+  if (L.copy_blocks > 0 && !evict_select_gathers(L) &&
       timed("evict_copy", s, [&] { return launch_evict_copy(L, s); }) != hipSuccess)
     return EBD_ERR_HIP;
   return EBD_OK;

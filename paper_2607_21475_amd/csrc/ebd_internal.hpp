@@ -140,6 +140,7 @@ size_t scores_workspace_bytes(int32_t U, int32_t nsplit, int32_t W);
 
 hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s);
 hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s);
+bool evict_select_gathers(const EvictLaunch &L);  // evict_select also gathers the rows (no copy launch)
 hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_attend_finalize(const AttendLaunch &L, hipStream_t s);
 hipError_t launch_append_certain(const AppendLaunch &L, hipStream_t s);

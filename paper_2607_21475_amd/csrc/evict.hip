@@ -1,21 +1,24 @@
 // evict.hip -- the Poisson tail sampler on gfx950 (Sec. 3.3: eq. (2), certainty set, Poisson tail;
 // Sec. 3.1: evicted rows are deleted, retained rows keep one stored pi each).
 //
-// Two launches per call:
+// Launches per call:
 //   evict_select_reg (units of at most 6144 tokens) one work-group of 2 waves per unit, the scores
 //                 in registers, so that every unit of a large batch is resident at once; the same
-//                 steps as evict_select below with one barrier per reduction or prefix.
+//                 steps as evict_select below with one barrier per reduction or prefix; then
+//                 evict_copy gathers the rows.
 //   evict_select  (longer units) one work-group of 8 waves per unit, two per CU.  Stages the
-//                 unit's scores in LDS (up to
-//                 16384 tokens, protected positions marked by a negative sentinel; longer units
-//                 are re-read from memory), solves lambda with sum_T clip(lambda s, eps, 1) = m by
-//                 safeguarded Newton steps on the piecewise linear g(lambda) (exact once the
-//                 piece is found), then walks the unit in blocks of 4 tokens per thread: Philox words and the
-//                 exact retention test (Poisson), or a block scan of the integer weights
-//                 ceil(pi 2^32) against one start per unit (fixed-size systematic design), or
-//                 the score threshold of a radix select (top-k comparison design); ballot ranks
-//                 plus a cross-wave prefix give the order in which the stored pi and original
-//                 position of every retained row are written, plus the count and status bits.
+//                 unit's scores in LDS (up to 16384 tokens, protected positions marked by a
+//                 negative sentinel; longer units are re-read from memory), solves lambda with
+//                 sum_T clip(lambda s, eps, 1) = m by safeguarded Newton steps on the piecewise
+//                 linear g(lambda) (exact once the piece is found), then walks the unit in blocks
+//                 of 4 tokens per thread: Philox words and the exact retention test (Poisson), or
+//                 a block scan of the integer weights ceil(pi 2^32) against one start per unit
+//                 (fixed-size systematic design), or the score threshold of a radix select (top-k
+//                 comparison design); ballot ranks plus a cross-wave prefix give the order in
+//                 which the stored pi and original position of every retained row are written,
+//                 plus the count and status bits.  The same work-group then gathers its unit's
+//                 retained K and V rows (these units run in many generations, so the gathers of
+//                 some overlap the selection of others; no second launch).
 //   evict_copy    one work-group per (unit, block of retained rows): gathers the retained K and
 //                 V rows named by the index list (16 lanes x 16 B per 256-byte row, all loads of
 //                 a thread in flight together, non-temporal loads and stores: every byte is
@@ -718,6 +721,48 @@ void evict_select_kernel(EvictLaunch L) {
     L.status[u] = st;
     if (L.lambda_out) L.lambda_out[u] = lamf;
   }
+
+  // The unit's retained K and V rows, gathered by the same work-group from the index list it
+  // has just written (visible to it after the barrier): 16 lanes per 256-byte row, 8 rows per
+  // thread with all their loads in flight, the next rows' indices loaded ahead.  Units of this
+  // kernel run in many generations, so one unit's gather overlaps other units' selection.
+  __syncthreads();
+  const int64_t nkeep = min(rank0, cap);
+  constexpr int kGRows = NT / 16, kGIt = 8;  // rows per pass, passes per round
+  const int sub = t & 15, grow = t >> 4;
+  const u32x4 *K4 = reinterpret_cast<const u32x4 *>(L.K);
+  const u32x4 *V4 = reinterpret_cast<const u32x4 *>(L.V);
+  u32x4 *Kc4 = reinterpret_cast<u32x4 *>(L.Kc);
+  u32x4 *Vc4 = reinterpret_cast<u32x4 *>(L.Vc);
+  // rows past the end re-load the unit's first retained row and skip the store
+  auto gather_idx = [&](int64_t r0, int32_t (&src)[kGIt]) {
+#pragma unroll
+    for (int k = 0; k < kGIt; ++k) {
+      const int64_t r = r0 + grow + k * kGRows;
+      src[k] = L.idxc[cbase + (r < nkeep ? r : 0)];
+    }
+  };
+  int32_t src[kGIt];
+  if (nkeep > 0) gather_idx(0, src);
+  for (int64_t r0 = 0; r0 < nkeep; r0 += kGRows * kGIt) {
+    u32x4 kv[kGIt], vv[kGIt];
+#pragma unroll
+    for (int k = 0; k < kGIt; ++k) {
+      const int64_t sr = (base + src[k]) * (kHeadDim / 8) + sub;
+      kv[k] = __builtin_nontemporal_load(&K4[sr]);  // streamed once: no cache retention
+      vv[k] = __builtin_nontemporal_load(&V4[sr]);
+    }
+    if (r0 + kGRows * kGIt < nkeep) gather_idx(r0 + kGRows * kGIt, src);
+#pragma unroll
+    for (int k = 0; k < kGIt; ++k) {
+      const int64_t r = r0 + grow + k * kGRows;
+      if (r < nkeep) {
+        const int64_t d = (cbase + r) * (kHeadDim / 8) + sub;
+        __builtin_nontemporal_store(kv[k], &Kc4[d]);
+        __builtin_nontemporal_store(vv[k], &Vc4[d]);
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1145,6 +1190,8 @@ hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s) {
   }
   return hipGetLastError();
 }
+
+bool evict_select_gathers(const EvictLaunch &L) { return (L.max_rows + 511) / 512 > 12; }
 
 hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)L.U * L.copy_blocks)), block(kCopyThreads);
