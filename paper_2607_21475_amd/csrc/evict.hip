@@ -319,6 +319,49 @@ __device__ uint32_t topk_threshold(double m, double n_tail, int *hist, int *sel,
 // ---------------------------------------------------------------------------------------------
 // evict_select: lambda, mask, stored pi and index of every retained row, count, status
 // ---------------------------------------------------------------------------------------------
+// The retained K and V rows of one unit, gathered in order by the NT threads of its work-group
+// from the index list (idxc) the work-group wrote: 16 lanes per 256-byte row, 8 rows per thread
+// with all their loads in flight, the next rows' indices loaded ahead.  Rows past the end
+// re-load the unit's first retained row and skip the store.
+template <int NT>
+__device__ __forceinline__ void gather_rows(const EvictLaunch &L, int64_t base, int64_t cbase,
+                                            int64_t nkeep) {
+  constexpr int kGRows = NT / 16, kGIt = 8;  // rows per pass, passes per round
+  const int t = threadIdx.x, sub = t & 15, grow = t >> 4;
+  const u32x4 *K4 = reinterpret_cast<const u32x4 *>(L.K);
+  const u32x4 *V4 = reinterpret_cast<const u32x4 *>(L.V);
+  u32x4 *Kc4 = reinterpret_cast<u32x4 *>(L.Kc);
+  u32x4 *Vc4 = reinterpret_cast<u32x4 *>(L.Vc);
+  auto load_idx = [&](int64_t r0, int32_t (&src)[kGIt]) {
+#pragma unroll
+    for (int k = 0; k < kGIt; ++k) {
+      const int64_t r = r0 + grow + k * kGRows;
+      src[k] = L.idxc[cbase + (r < nkeep ? r : 0)];
+    }
+  };
+  int32_t src[kGIt];
+  if (nkeep > 0) load_idx(0, src);
+  for (int64_t r0 = 0; r0 < nkeep; r0 += kGRows * kGIt) {
+    u32x4 kv[kGIt], vv[kGIt];
+#pragma unroll
+    for (int k = 0; k < kGIt; ++k) {
+      const int64_t sr = (base + src[k]) * (kHeadDim / 8) + sub;
+      kv[k] = __builtin_nontemporal_load(&K4[sr]);  // streamed once: no cache retention
+      vv[k] = __builtin_nontemporal_load(&V4[sr]);
+    }
+    if (r0 + kGRows * kGIt < nkeep) load_idx(r0 + kGRows * kGIt, src);
+#pragma unroll
+    for (int k = 0; k < kGIt; ++k) {
+      const int64_t r = r0 + grow + k * kGRows;
+      if (r < nkeep) {
+        const int64_t d = (cbase + r) * (kHeadDim / 8) + sub;
+        __builtin_nontemporal_store(kv[k], &Kc4[d]);
+        __builtin_nontemporal_store(vv[k], &Vc4[d]);
+      }
+    }
+  }
+}
+
 template <int NT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4)))
 void evict_select_kernel(EvictLaunch L) {
@@ -723,46 +766,10 @@ void evict_select_kernel(EvictLaunch L) {
   }
 
   // The unit's retained K and V rows, gathered by the same work-group from the index list it
-  // has just written (visible to it after the barrier): 16 lanes per 256-byte row, 8 rows per
-  // thread with all their loads in flight, the next rows' indices loaded ahead.  Units of this
-  // kernel run in many generations, so one unit's gather overlaps other units' selection.
+  // has just written (visible to it after the barrier).  Units of this kernel run in many
+  // generations, so one unit's gather overlaps other units' selection.
   __syncthreads();
-  const int64_t nkeep = min(rank0, cap);
-  constexpr int kGRows = NT / 16, kGIt = 8;  // rows per pass, passes per round
-  const int sub = t & 15, grow = t >> 4;
-  const u32x4 *K4 = reinterpret_cast<const u32x4 *>(L.K);
-  const u32x4 *V4 = reinterpret_cast<const u32x4 *>(L.V);
-  u32x4 *Kc4 = reinterpret_cast<u32x4 *>(L.Kc);
-  u32x4 *Vc4 = reinterpret_cast<u32x4 *>(L.Vc);
-  // rows past the end re-load the unit's first retained row and skip the store
-  auto gather_idx = [&](int64_t r0, int32_t (&src)[kGIt]) {
-#pragma unroll
-    for (int k = 0; k < kGIt; ++k) {
-      const int64_t r = r0 + grow + k * kGRows;
-      src[k] = L.idxc[cbase + (r < nkeep ? r : 0)];
-    }
-  };
-  int32_t src[kGIt];
-  if (nkeep > 0) gather_idx(0, src);
-  for (int64_t r0 = 0; r0 < nkeep; r0 += kGRows * kGIt) {
-    u32x4 kv[kGIt], vv[kGIt];
-#pragma unroll
-    for (int k = 0; k < kGIt; ++k) {
-      const int64_t sr = (base + src[k]) * (kHeadDim / 8) + sub;
-      kv[k] = __builtin_nontemporal_load(&K4[sr]);  // streamed once: no cache retention
-      vv[k] = __builtin_nontemporal_load(&V4[sr]);
-    }
-    if (r0 + kGRows * kGIt < nkeep) gather_idx(r0 + kGRows * kGIt, src);
-#pragma unroll
-    for (int k = 0; k < kGIt; ++k) {
-      const int64_t r = r0 + grow + k * kGRows;
-      if (r < nkeep) {
-        const int64_t d = (cbase + r) * (kHeadDim / 8) + sub;
-        __builtin_nontemporal_store(kv[k], &Kc4[d]);
-        __builtin_nontemporal_store(vv[k], &Vc4[d]);
-      }
-    }
-  }
+  gather_rows<NT>(L, base, cbase, min(rank0, cap));
 }
 
 // ---------------------------------------------------------------------------------------------
