@@ -55,13 +55,14 @@ def load_traffic(workload: str, kernel: str):
     return None if k is None else k.get("bytes_per_launch")
 
 
-def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str) -> int:
+def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str,
+                  out_dir: str = "") -> int:
     """Per-launch HBM bytes of the library's kernels from two rocprofv3 --pmc csv runs.
 
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same counter reads
     for the 1 GiB device copy that --copy-calibration runs (1 GiB read, 1 GiB written).
     Writes profiles/hbm_traffic_<workload>.json (read by the benchmark while the kernel sources
-    are unchanged) and a short text summary next to it.
+    are unchanged), or the same file under out_dir.
     """
     import csv
     import glob
@@ -99,8 +100,9 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str) -
                       "launches_profiled": len(fetch.get(k, []))}
     rec = {"workload": workload, "kernel_sources_hash": kernel_sources_hash(),
            "fetch_scale": fscale, "write_scale": wscale, "kernels": kernels, "command": command}
-    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % workload)
+    out_dir = out_dir or os.path.join(ROOT, "profiles")
+    os.makedirs(out_dir, exist_ok=True)
+    path = os.path.join(out_dir, "hbm_traffic_%s.json" % workload)
     json.dump(rec, open(path, "w"), indent=1)
     print(json.dumps(rec, indent=1))
     return 0
