@@ -128,6 +128,8 @@ def main() -> int:
     ap.add_argument("--compare-arms", action="store_true",
                     help="instead of timing: errors of the sampling designs against full attention")
     ap.add_argument("--compare-units", type=int, default=256)
+    ap.add_argument("--next-steps", type=int, default=3,
+                    help="timed repetitions of the rows built after the hot path (0: skip)")
     args = ap.parse_args()
 
     if args.summarize_pmc:
@@ -321,6 +323,8 @@ def main() -> int:
         imp["gbs"] = round(sum(sb.values()) * args.scores_steps / (tot_ms * 1e-3) / 1e9, 1)
         del qw, sws, sco
 
+    nxt = next_rows(args, wl, inp, plans, ebd, torch) if args.next_steps > 0 else None
+
     # CPU baseline: the fp64 oracle on a bounded sample of the same units, same budgets.
     cpu = None
     if args.cpu_seconds > 0:
@@ -353,10 +357,80 @@ def main() -> int:
         "roofline": roofline,
         "cpu_baseline": cpu,
         "importance_scores": imp,
+        "next_rows": nxt,
         "kernel_sources_hash": kernel_sources_hash(),
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+def next_rows(args, wl, inp, plans, ebd, torch):
+    """Timing of the rows built after the hot path, on the benchmark's own inputs: the
+    per-block variance contributions and the deployed certificate step over the middle budget's
+    retained caches and attention outputs, then the other sampling designs (fixed-size
+    systematic, top-k, uniform) evicting the same units at every budget."""
+    U, n, G = wl.units, wl.context, wl.group
+    res = {}
+    p = plans[len(plans) // 2]
+    rc, o = p["rc"], p["out"]
+    retained = int(rc.count.sum().item())
+    nblocks = (n + 63) // 64
+    blocks = torch.empty((U, nblocks), dtype=torch.float32, device="cuda")
+    # units are (layer, sequence, KV head) with the KV head fastest; each holds G query heads
+    useq = torch.tensor([(u // wl.kv_heads) % wl.batch for u in range(U)], dtype=torch.int32,
+                        device="cuda")
+    uh0 = torch.tensor([(u % wl.kv_heads) * G for u in range(U)], dtype=torch.int32, device="cuda")
+    cert = torch.zeros(wl.batch, dtype=torch.float32, device="cuda")
+    ebd.ebd_block_contributions(U, G, nblocks, rc.max_cap, rc.cap_off, inp["q"], rc.Kc, rc.Vc,
+                                rc.pic, rc.idxc, rc.count, o["y"], o["lse"], blocks)
+    torch.cuda.synchronize()
+    ebd.ebd_timing_enable(True)
+    for k in ("block_contrib", "cert_step"):
+        ebd.ebd_timing_read(k)
+    for _ in range(args.next_steps):
+        ebd.ebd_block_contributions(U, G, nblocks, rc.max_cap, rc.cap_off, inp["q"], rc.Kc, rc.Vc,
+                                    rc.pic, rc.idxc, rc.count, o["y"], o["lse"], blocks)
+        ebd.ebd_certificate_step(U, G, wl.batch, useq, o["r"], cert, unit_head0=uh0)
+    torch.cuda.synchronize()
+    bc, cs = ebd.ebd_timing_read("block_contrib"), ebd.ebd_timing_read("cert_step")
+    bc_us = bc[0] / max(bc[1], 1) * 1e3
+    bbytes = 520 * retained * ((G + 7) // 8)  # K, V, pi, index per retained row and head block
+    res["block_contrib"] = {"budget": p["budget"], "avg_us": round(bc_us, 2),
+                            "alg_bytes_per_launch": bbytes,
+                            "achieved_gbs": round(bbytes / (bc_us * 1e-6) / 1e9, 1),
+                            "frac_hbm": round(bbytes / (bc_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    res["cert_step"] = {"avg_us": round(cs[0] / max(cs[1], 1) * 1e3, 2), "sequences": wl.batch}
+    designs = {}
+    for name, design in (("systematic", ebd.EBD_DESIGN_SYSTEMATIC), ("topk", ebd.EBD_DESIGN_TOPK),
+                         ("uniform", ebd.EBD_DESIGN_UNIFORM)):
+        eps = [ebd.evict_params(U, n, q["rc"].max_cap, inp["seq_off"], q["rc"].cap_off, wl.n_sink,
+                                wl.n_recent, q["budget"], None, wl.pi_min, 0, args.seed, None, 0,
+                                design) for q in plans]
+
+        def evict_all():
+            for q, ep in zip(plans, eps):
+                r = q["rc"]
+                ebd.ebd_evict(ep, inp["scores"], inp["K"], inp["V"], r.Kc, r.Vc, r.pic, r.idxc,
+                              r.count, r.status, q["ews"])
+
+        evict_all()
+        torch.cuda.synchronize()
+        for k in ("evict_select", "evict_copy"):
+            ebd.ebd_timing_read(k)
+        for _ in range(args.next_steps):
+            evict_all()
+        torch.cuda.synchronize()
+        ms = sum(ebd.ebd_timing_read(k)[0] for k in ("evict_select", "evict_copy"))
+        calls = args.next_steps * len(plans)
+        overflow = any(bool((q["rc"].status.cpu().numpy() & ebd.EBD_ST_CAP_OVERFLOW).any())
+                       for q in plans)
+        designs[name] = {"evict_us_per_call": round(ms / calls * 1e3, 2),
+                         "evictions_per_s": round(U * calls / (ms * 1e-3), 1),
+                         "retained_rows": [int(q["rc"].count.sum().item()) for q in plans],
+                         "capacity_overflow": overflow}
+    ebd.ebd_timing_enable(False)
+    res["designs"] = designs
+    return res
 
 
 def compare_arms(args, wl, budgets) -> int:

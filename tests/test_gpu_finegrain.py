@@ -72,6 +72,55 @@ def test_block_contributions(lengths, G, budget, block_rows):
             assert abs(got[u].sum() - vh[u].sum()) <= 1e-2 * vh[u].sum() + 1e-30
 
 
+def test_block_contributions_dominant_row():
+    """One tail row takes almost all the attention of every head, so yhat is close to its value
+    row and |v - yhat|^2 = |v|^2 - 2 yhat.v + |yhat|^2 cancels: the kernel must fall back to the
+    direct sum there."""
+    _say("block contributions, dominant row")
+    import paper_2607_21475_amd as ebd
+    from paper_2607_21475_amd import cache
+
+    lengths = [2048, 2048]
+    U, G, block_rows = len(lengths), 4, 64
+    K, V, seq_off = synth.make_cache(lengths, seed=51, device="cuda")
+    K = (K.float() * 0.05).to(torch.bfloat16)
+    q1 = synth.make_queries(U, 1, seed=52, device="cuda")
+    q = q1.expand(U, G, 128).contiguous()  # the same query for every head
+    for u in range(U):
+        K[u * 2048 + 1000] = (q1[u, 0].float() * 2.0).to(torch.bfloat16)
+    # at a 50% budget the unit scores give lambda ~ 0.483, so row 1000 (score 2.07) gets
+    # pi ~ 0.999: kept in practice, yet a tail row with a nonzero variance term
+    sc = torch.ones(U * 2048, dtype=torch.float32, device="cuda")
+    for u in range(U):
+        sc[u * 2048 + 1000] = 2.07
+    out = cache.evict(K, V, sc, seq_off, lengths, budget_frac=0.5, seed=3)
+    idx = _np(out.idxc)
+    coff, cnt = _np(out.cap_off), _np(out.count)
+    for u in range(U):
+        a, c = coff[u], int(min(cnt[u], coff[u + 1] - coff[u]))
+        if 1000 not in set(idx[a:a + c].tolist()):
+            pytest.skip("row 1000 was not drawn for unit %d" % u)
+    res = cache.attend_certify(out, q)
+    nb = 2048 // block_rows
+    blocks = torch.empty((U, nb), dtype=torch.float32, device="cuda")
+    ebd.ebd_block_contributions(U, G, nb, out.max_cap, out.cap_off, q, out.Kc, out.Vc, out.pic,
+                                out.idxc, out.count, res["y"], res["lse"], blocks,
+                                block_rows=block_rows)
+    torch.cuda.synchronize()
+    got = _np(blocks).astype(np.float64)
+    bits = synth.bf16_bits
+    for u in range(U):
+        a, c = coff[u], int(min(cnt[u], coff[u + 1] - coff[u]))
+        ref = oracle.block_contributions(bits(q[u]), bits(out.Kc[a:a + c]), bits(out.Vc[a:a + c]),
+                                         _np(out.pic[a:a + c]), _np(out.idxc[a:a + c]),
+                                         _np(res["y"][u]).astype(np.float64),
+                                         _np(res["lse"][u]).astype(np.float64), nb, block_rows)
+        b0 = 1000 // block_rows
+        assert abs(got[u, b0] - ref[b0]) <= 1e-3 * abs(ref[b0]) + 1e-30, (got[u, b0], ref[b0])
+        tol = 1e-3 * np.abs(ref) + 1e-7 * max(ref.max(initial=0.0), 1e-30)
+        assert np.all(np.abs(got[u] - ref) <= tol)
+
+
 def test_certificate_step_over_decode_steps():
     _say("certificate step")
     import paper_2607_21475_amd as ebd
