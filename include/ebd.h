@@ -272,7 +272,8 @@ ebd_status ebd_block_contributions(const ebd_blocks_params *p, const uint16_t *q
  * head_stride; cert[s] = max(cert[s], mean) (the caller sets cert before the first step);
  * mean_out[s] (or NULL) receives the mean.  A sequence without sampled pairs keeps cert[s]
  * and gets mean 0.  unit_seq [U] device int32 (negative: not counted); unit_head0 [U] device
- * int32 or NULL (all 0); radius [U, G] as written by ebd_attend_certify.
+ * int32 >= 0 or NULL (all 0); radius [U, G] as written by ebd_attend_certify.  U G < 2^31
+ * (else EBD_ERR_INVALID_ARG).  The sums are taken in a fixed order (deterministic).
  */
 typedef struct ebd_cert_params {
     int32_t num_units;

@@ -391,7 +391,8 @@ ebd_status ebd_block_contributions(const ebd_blocks_params *p, const uint16_t *q
 
 ebd_status ebd_certificate_step(const ebd_cert_params *p, const float *radius, float *cert,
                                 float *mean_out, void *stream) {
-  if (!p || p->num_units < 0 || p->group < 1 || p->num_seqs < 0 || p->head_stride < 1)
+  if (!p || p->num_units < 0 || p->group < 1 || p->num_seqs < 0 || p->head_stride < 1 ||
+      (int64_t)p->num_units * p->group >= ((int64_t)1 << 31))
     return EBD_ERR_INVALID_ARG;
   if (p->num_seqs == 0) return EBD_OK;
   if (!cert || (p->num_units > 0 && (!p->unit_seq || !radius))) return EBD_ERR_INVALID_ARG;

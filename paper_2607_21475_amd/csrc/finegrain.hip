@@ -219,20 +219,42 @@ __global__ __launch_bounds__(64, 2) void block_contrib_kernel(BlocksLaunch L, in
   for (int64_t b = lane; b < L.nblocks; b += 64) out[b] = (h0 == 0 ? 0.0f : out[b]) + s_bin[b];
 }
 
-__global__ __launch_bounds__(256) void cert_step_kernel(CertLaunch L) {
-  __shared__ double s_sum[4];
-  __shared__ int s_cnt[4];
+constexpr int kCertThreads = 1024;
+
+__global__ __launch_bounds__(kCertThreads) void cert_step_kernel(CertLaunch L) {
+  constexpr int NW = kCertThreads / 64;
+  __shared__ double s_sum[NW];
+  __shared__ int s_cnt[NW];
   const int sq = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   double sum = 0.0;
   int cnt = 0;
-  for (int u = t; u < L.U; u += 256) {
-    if (L.unit_seq[u] != sq) continue;
-    const int64_t h0 = L.unit_head0 ? L.unit_head0[u] : 0;
-    for (int g = 0; g < L.G; ++g) {
-      if ((h0 + g) % L.head_stride != 0) continue;
-      sum += (double)L.radius[(int64_t)u * L.G + g];
-      ++cnt;
+  // (unit, head) pairs e = u G + g spread over the threads, up to eight per thread with all their
+  // reads issued together (walked by unit, a sequence's units can all fall to a few threads);
+  // 32-bit indices (the call checks U G < 2^31)
+  const uint32_t total = (uint32_t)L.U * (uint32_t)L.G, G = (uint32_t)L.G;
+  const uint32_t stride = (uint32_t)L.head_stride;
+  constexpr int kB = 8;
+  for (uint32_t e0 = (uint32_t)t; e0 < total; e0 += (uint32_t)kCertThreads * kB) {
+    int seq[kB];
+    uint32_t hg[kB];
+    float rv[kB];
+#pragma unroll
+    for (int k = 0; k < kB; ++k) {
+      const uint32_t e = e0 + (uint32_t)kCertThreads * k;
+      const bool in = e < total;
+      const uint32_t u = in ? e / G : 0u;
+      seq[k] = in ? L.unit_seq[u] : -1;
+      const uint32_t h0 = (in && L.unit_head0) ? (uint32_t)L.unit_head0[u] : 0u;
+      hg[k] = h0 + (e - u * G);  // the head's index in its layer
+      rv[k] = in ? L.radius[e] : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < kB; ++k) {
+      if (seq[k] == sq && hg[k] % stride == 0u) {
+        sum += (double)rv[k];
+        ++cnt;
+      }
     }
   }
   sum = wave_sum(sum);
@@ -243,9 +265,13 @@ __global__ __launch_bounds__(256) void cert_step_kernel(CertLaunch L) {
   }
   __syncthreads();
   if (t == 0) {
-    const double total = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
-    const int n = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
-    const float mean = n > 0 ? (float)(total / (double)n) : 0.0f;
+    double tsum = 0.0;
+    int n = 0;
+    for (int w = 0; w < NW; ++w) {
+      tsum += s_sum[w];
+      n += s_cnt[w];
+    }
+    const float mean = n > 0 ? (float)(tsum / (double)n) : 0.0f;
     if (L.mean_out) L.mean_out[sq] = mean;
     if (n > 0) L.cert[sq] = fmaxf(L.cert[sq], mean);
   }
@@ -277,7 +303,7 @@ hipError_t launch_block_contrib(const BlocksLaunch &L, hipStream_t s) {
 }
 
 hipError_t launch_cert_step(const CertLaunch &L, hipStream_t s) {
-  hipLaunchKernelGGL(cert_step_kernel, dim3((unsigned)L.S), dim3(256), 0, s, L);
+  hipLaunchKernelGGL(cert_step_kernel, dim3((unsigned)L.S), dim3(kCertThreads), 0, s, L);
   return hipGetLastError();
 }
 

@@ -223,6 +223,9 @@ def test_finegrain_argument_validation():
     assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, FAKE, None, None) == ebd.EBD_ERR_INVALID_ARG
     c.head_stride = 4
     assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, None, None, None) == ebd.EBD_ERR_INVALID_ARG
+    c.num_units, c.group = 1 << 28, 8  # U G >= 2^31
+    assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, FAKE, None, None) == ebd.EBD_ERR_INVALID_ARG
+    c.num_units, c.group = 4, 7
     c.num_seqs = 0
     assert lib.ebd_certificate_step(ctypes.byref(c), FAKE, FAKE, None, None) == ebd.EBD_OK
 
