@@ -515,6 +515,25 @@ def test_qwen7b_full_size_sampled_units():
             for key in ("vhat", "b", "r"):
                 g = _np(res[key][u]).astype(np.float64)
                 assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.abs(ref[key])), (key, u, g, ref[key])
+        if budget == 0.25:  # the benchmark's block-contribution launch, sampled units
+            import paper_2607_21475_amd as ebd
+
+            nb = (n + 63) // 64
+            blocks = torch.empty((wl.units, nb), dtype=torch.float32, device="cuda")
+            ebd.ebd_block_contributions(wl.units, wl.group, nb, out.max_cap, out.cap_off, inp["q"],
+                                        out.Kc, out.Vc, out.pic, out.idxc, out.count, res["y"],
+                                        res["lse"], blocks)
+            torch.cuda.synchronize()
+            got = _np(blocks).astype(np.float64)
+            for u in sample[:4]:
+                a, c = coff[u], int(cnt[u])
+                bref = oracle.block_contributions(
+                    _bits(inp["q"][u]), _bits(out.Kc[a:a + c]), _bits(out.Vc[a:a + c]),
+                    _np(out.pic[a:a + c]), _np(out.idxc[a:a + c]),
+                    _np(res["y"][u]).astype(np.float64), _np(res["lse"][u]).astype(np.float64),
+                    nb, 64)
+                tol = 1e-3 * np.abs(bref) + 1e-7 * max(bref.max(initial=0.0), 1e-30)
+                assert np.all(np.abs(got[u] - bref) <= tol), u
         del out, res
     del inp
     torch.cuda.empty_cache()
