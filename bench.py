@@ -130,6 +130,9 @@ def main() -> int:
     ap.add_argument("--compare-units", type=int, default=256)
     ap.add_argument("--next-steps", type=int, default=3,
                     help="timed repetitions of the rows built after the hot path (0: skip)")
+    ap.add_argument("--replay-chunk", type=int, default=-1, metavar="CHUNK",
+                    help="instead of a workload: time one chunk (0..7) of 1512 cells of the replay "
+                         "grid (8 KV heads per cell, G = 1, per-unit budgets and contexts)")
     args = ap.parse_args()
 
     if args.summarize_pmc:
@@ -155,6 +158,8 @@ def main() -> int:
     budgets = [float(b) for b in args.budgets.split(",")] if args.budgets else list(wl.budgets)
     if args.compare_arms:
         return compare_arms(args, wl, budgets)
+    if args.replay_chunk >= 0:
+        return replay_chunk(args)
     U, n, G = wl.units, wl.context, wl.group
     lengths = [n] * U
 
@@ -431,6 +436,64 @@ def next_rows(args, wl, inp, plans, ebd, torch):
     ebd.ebd_timing_enable(False)
     res["designs"] = designs
     return res
+
+
+def replay_chunk(args) -> int:
+    """One chunk of the replay grid as one eviction and one certified decode step: cells
+    c0 .. c0 + 1511 (c0 = 1512 x chunk), 8 KV heads each (G = 1), every cell with its own budget
+    (5 .. 50%) and context (2048 / 6144 / 16384); its full caches (about 50 GB) fit one GPU, the
+    whole grid's (406 GB) are evicted chunk by chunk."""
+    import torch
+
+    import synth
+    import paper_2607_21475_amd as ebd
+    from paper_2607_21475_amd import cache
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    ncell = 1512
+    c0 = ncell * args.replay_chunk
+    cells = [synth.replay_cell(c) for c in range(c0, c0 + ncell)]
+    H = synth.REPLAY_KV_HEADS
+    lengths = [ctx for (_, ctx, _, _) in cells for _ in range(H)]
+    budgets = [b for (b, _, _, _) in cells for _ in range(H)]
+    U = len(lengths)
+    K, V, seq_off = synth.make_cache(lengths, seed=args.seed + 5, device="cuda")
+    sc = synth.window_scores(K, seq_off, seed=args.seed + 6)
+    q = synth.make_queries(U, 1, seed=args.seed + 7, device="cuda")
+    bpu = torch.tensor(budgets, dtype=torch.float32, device="cuda")
+    out = cache.evict(K, V, sc, seq_off, lengths, budget_per_unit=bpu, seed=args.seed)
+    res = cache.attend_certify(out, q)
+    torch.cuda.synchronize()
+    if (out.status.cpu().numpy() & ebd.EBD_ST_CAP_OVERFLOW).any():
+        raise RuntimeError("capacity overflow in the replay chunk")
+    retained = int(out.count.sum().item())
+    names = ("evict_select", "evict_copy", "attend_split", "attend_finalize")
+    ebd.ebd_timing_enable(True)
+    for k in names:
+        ebd.ebd_timing_read(k)
+    for _ in range(args.steps):
+        out2 = cache.evict(K, V, sc, seq_off, lengths, budget_per_unit=bpu, seed=args.seed)
+        del out2
+        cache.attend_certify(out, q, ws=res["ws"])
+    torch.cuda.synchronize()
+    t = {k: ebd.ebd_timing_read(k) for k in names}
+    ebd.ebd_timing_enable(False)
+    att_ms = (t["attend_split"][0] + t["attend_finalize"][0]) / args.steps
+    ev_ms = (t["evict_select"][0] + t["evict_copy"][0]) / args.steps
+    kv = 512 * retained
+    line = {"mode": "replay_chunk", "chunk": args.replay_chunk, "cells": ncell, "units": U,
+            "group": 1, "rows": int(sum(lengths)), "retained_rows": retained, "steps": args.steps,
+            "attend_us": round(att_ms * 1e3, 1),
+            "attend_launches_per_call": {k: t[k][1] // args.steps for k in names[2:]},
+            "retained_kv_gbs": round(kv / (att_ms * 1e-3) / 1e9, 1),
+            "retained_kv_frac_hbm": round(kv / (att_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "evict_us": round(ev_ms * 1e3, 1),
+            "evict_launches_per_call": {k: t[k][1] // args.steps for k in names[:2]},
+            "evictions_per_s": round(U / (ev_ms * 1e-3), 1),
+            "evict_gbs": round((4 * sum(lengths) + 1032 * retained) / (ev_ms * 1e-3) / 1e9, 1)}
+    print(json.dumps(line), flush=True)
+    return 0
 
 
 def compare_arms(args, wl, budgets) -> int:
