@@ -246,7 +246,8 @@ ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint1
  *   y, lse: the outputs of ebd_attend_certify for the same q (yhat and ln Nhat).
  *   Rows with pi = 1, with idxc < 0 (appended decode rows) or past the last block add nothing.
  *   block_rows >= 1; 1 <= nblocks <= 8192; max_rows as for ebd_attend_certify (rows of a unit
- *   beyond it are ignored).  blocks [U, nblocks] fp32 is written.  No workspace.
+ *   beyond it are ignored), at most 2^24 (else EBD_ERR_UNSUPPORTED).  blocks [U, nblocks] fp32
+ *   is written.  No workspace.
  */
 typedef struct ebd_blocks_params {
     int32_t num_units;

@@ -359,6 +359,7 @@ ebd_status ebd_block_contributions(const ebd_blocks_params *p, const uint16_t *q
       p->nblocks > kMaxBlocks || p->max_rows < 0 || p->scale < 0.0f || !std::isfinite(p->scale))
     return EBD_ERR_INVALID_ARG;
   if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  if (p->max_rows > ((int64_t)1 << 24)) return EBD_ERR_UNSUPPORTED;  // one wave reads a unit
   if (p->num_units == 0) return EBD_OK;
   if (!p->cap_off || !q || !Kc || !Vc || !pic || !idxc || !count || !y || !lse || !blocks)
     return EBD_ERR_INVALID_ARG;

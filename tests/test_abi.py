@@ -207,7 +207,8 @@ def test_finegrain_argument_validation():
     def bp(**kw):
         p = ebd.ebd_blocks_params()
         p.num_units, p.group, p.head_dim = kw.get("U", 4), kw.get("G", 7), kw.get("d", 128)
-        p.block_rows, p.nblocks, p.max_rows = kw.get("rows", 64), kw.get("nb", 96), 4096
+        p.block_rows, p.nblocks = kw.get("rows", 64), kw.get("nb", 96)
+        p.max_rows = kw.get("max_rows", 4096)
         p.cap_off = FAKE
         return p
 
@@ -217,6 +218,7 @@ def test_finegrain_argument_validation():
     assert call(bp(d=64)) == ebd.EBD_ERR_UNSUPPORTED
     for bad in (dict(G=0), dict(rows=0), dict(nb=0), dict(nb=8193), dict(U=-1)):
         assert call(bp(**bad)) == ebd.EBD_ERR_INVALID_ARG, bad
+    assert call(bp(max_rows=(1 << 24) + 1)) == ebd.EBD_ERR_UNSUPPORTED
     assert call(bp(U=0)) == ebd.EBD_OK
     c = ebd.ebd_cert_params()
     c.num_units, c.group, c.num_seqs, c.head_stride, c.unit_seq = 4, 7, 2, 0, FAKE
