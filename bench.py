@@ -208,6 +208,16 @@ def main() -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # which budgets' evictions gather their rows inside evict_select (no evict_copy launch)
+    ebd.ebd_timing_enable(True)
+    for p in plans:
+        ebd.ebd_timing_read("evict_copy")
+        rc = p["rc"]
+        ebd.ebd_evict(p["ep"], inp["scores"], inp["K"], inp["V"], rc.Kc, rc.Vc, rc.pic, rc.idxc,
+                      rc.count, rc.status, p["ews"])
+        torch.cuda.synchronize()
+        p["gathers"] = ebd.ebd_timing_read("evict_copy")[1] == 0
+    ebd.ebd_timing_enable(False)
     for p in plans:
         st = p["rc"].status.cpu().numpy()
         if (st & ebd.EBD_ST_CAP_OVERFLOW).any():
@@ -230,30 +240,33 @@ def main() -> int:
     # Work per step, from the (deterministic) retained counts.
     per_budget = []
     retained_total = 0
+    gathered = 0  # retained rows of budgets whose evict_select also gathers
     for p in plans:
         cnt = p["rc"].count.cpu().numpy().astype(np.int64)
         rescans = cache.rescans(p["aws"], U, G)
         per_budget.append(dict(budget=p["budget"], retained_rows=int(cnt.sum()),
                                mean_retained_per_unit=float(cnt.mean()),
-                               range_term_rescans=int(rescans), fused_finalize=bool(p["fused"])))
+                               range_term_rescans=int(rescans), fused_finalize=bool(p["fused"]),
+                               select_gathers=bool(p["gathers"])))
         retained_total += int(cnt.sum())
+        if p["gathers"]:
+            gathered += int(cnt.sum())
     K = args.steps
     nb = len(plans)
     kv_bytes = 512 * retained_total  # K + V bf16 rows retained, per step (all budgets)
     nfused = sum(1 for p in plans if p["fused"])
     alg = {
-        # scores read once per cached token; pi and index written per retained row
-        "evict_select": 4 * U * n * nb + 8 * retained_total,
+        # scores read once per cached token; pi and index written per retained row; rows read and
+        # written (1024 B) where the selection also gathers them
+        "evict_select": 4 * U * n * nb + 8 * retained_total + 1024 * gathered,
         # read K+V rows (512 B) and write Kc+Vc rows (512 B) per retained row
-        "evict_copy": 1024 * retained_total,
+        "evict_copy": 1024 * (retained_total - gathered),
         # K, V, pi per retained row (516 B) and the query heads; a split kernel that finalizes
         # its units itself also writes y (512 B), vhat, lse, b, r per query head
         "attend_split": 516 * retained_total + nb * U * G * 256 + nfused * U * G * (512 + 16),
         # y, vhat, lse, b, r per query head of budgets whose units span several splits
         "attend_finalize": (nb - nfused) * U * G * (512 + 16),
     }
-    if kt["evict_copy"][1] == 0:  # units past the register sampler: evict_select gathers the rows
-        alg["evict_select"] += alg["evict_copy"]
     kern = {}
     for k in KERNELS:
         ms, launches = kt[k]
