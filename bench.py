@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import math
 import os
@@ -35,11 +36,16 @@ KERNELS = ("evict_select", "evict_copy", "attend_split", "attend_finalize")
 
 
 def kernel_sources_hash() -> str:
+    """Hash of the library sources with comments and blank space removed (a comment edit does not
+    make the committed counter summary stale; any code change does)."""
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2607_21475_amd", "csrc")
     for f in sorted(os.listdir(d)):
         if f.endswith((".hip", ".hpp", ".cpp")):
-            h.update(open(os.path.join(d, f), "rb").read())
+            src = open(os.path.join(d, f)).read()
+            src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)  # block comments
+            src = re.sub(r"//[^\n]*", "", src)  # line comments
+            h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 

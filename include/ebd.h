@@ -123,8 +123,9 @@ typedef struct ebd_evict_params {
  *     status [U] uint32             EBD_ST_* bits
  *   workspace: at least ebd_workspace_size(EBD_WS_EVICT, p) bytes, 256-byte aligned
  *   (currently reserved: the sampler's launches share only the idxc list they write).
- *   Units of at most 6144 tokens take two launches (selection, then the row gather
- *   "evict_copy"); longer units one ("evict_select" also gathers the rows).
+ *   Launches whose units are at most 6144 tokens long, with capacities of at least a sixth
+ *   of that, take two kernels (selection, then the row gather "evict_copy"); other launches
+ *   one ("evict_select" also gathers the rows).
  *   Rows of Kc/Vc/pic/idxc beyond count[u] are left untouched.
  */
 ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint16_t *K,

@@ -2,11 +2,11 @@
 // Sec. 3.1: evicted rows are deleted, retained rows keep one stored pi each).
 //
 // Launches per call:
-//   evict_select_reg (units of at most 6144 tokens) one work-group of 2 waves per unit, the scores
-//                 in registers, so that every unit of a large batch is resident at once; the same
-//                 steps as evict_select below with one barrier per reduction or prefix; then
-//                 evict_copy gathers the rows.
-//   evict_select  (longer units) one work-group of 8 waves per unit, two per CU.  Stages the
+//   evict_select_reg (units of at most 6144 tokens with a capacity of at least a sixth of their
+//                 length) one work-group of 2 waves per unit, the scores in registers, so that
+//                 every unit of a large batch is resident at once; the same steps as evict_select
+//                 below with one barrier per reduction or prefix; then evict_copy gathers the rows.
+//   evict_select  (every other launch) one work-group of 8 waves per unit, two per CU.  Stages the
 //                 unit's scores in LDS (up to 16384 tokens, protected positions marked by a
 //                 negative sentinel; longer units are re-read from memory), solves lambda with
 //                 sum_T clip(lambda s, eps, 1) = m by safeguarded Newton steps on the piecewise
@@ -17,8 +17,8 @@
 //                 comparison design); ballot ranks plus a cross-wave prefix give the order in
 //                 which the stored pi and original position of every retained row are written,
 //                 plus the count and status bits.  The same work-group then gathers its unit's
-//                 retained K and V rows (these units run in many generations, so the gathers of
-//                 some overlap the selection of others; no second launch).
+//                 retained K and V rows (the gathers of some units overlap the selection of
+//                 others; no second launch).
 //   evict_copy    one work-group per (unit, block of retained rows): gathers the retained K and
 //                 V rows named by the index list (16 lanes x 16 B per 256-byte row, all loads of
 //                 a thread in flight together, non-temporal loads and stores: every byte is
