@@ -36,7 +36,8 @@ extern "C" {
 typedef enum ebd_status {
     EBD_OK = 0,
     EBD_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, bad parameter */
-    EBD_ERR_UNSUPPORTED = 2, /* head_dim != 128, or no gfx950 device current */
+    EBD_ERR_UNSUPPORTED = 2, /* head_dim != 128, no gfx950 device current, or a size beyond
+                                a limit documented at the entry point */
     EBD_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than ebd_workspace_size() */
     EBD_ERR_HIP = 4          /* a HIP runtime call failed (launch, event) */
 } ebd_status;
