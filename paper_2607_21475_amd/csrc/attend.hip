@@ -20,8 +20,9 @@
 //   o = sum w v (rows < GB) and Cv = sum c v (rows GB..2GB-1) together, with V in its natural
 //   row-major layout (no transpose): each fp32 weight enters as an exact three-term bf16 sum,
 //   so every product is exact and only the fp32 sums round.
-//   Range-term candidates, per 512-row chunk: weight lanes take the rows of even tiles and
-//   variance lanes (same logits) those of odd tiles; each lane keeps its four largest
+//   Range-term candidates, per 512-row chunk: in every tile the weight lane of a head takes
+//   rows 0 and 1 of its 4-row group and the variance lane (same logits) rows 2 and 3; each lane
+//   keeps its four largest
 //   g^2 |v|^2 (g^2 = (1 - pi) w^2) plus the maxima of g |v| and of g over what it dropped, so
 //   a chunk holds 32 candidates per head with bounds for the rest.
 //   The running max m moves lazily (only by jumps of more than 2^8 in weight).
@@ -87,8 +88,8 @@ constexpr float kLazy = 8.0f;
 // One 16-row tile: rows 16t + 4g + i of the split for this lane's head slot; `nvalid` rows of the
 // lane's row group are real (<= 0 masks them all), `rowbase` is the unit row of its first one.
 __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const bf16x8 (&qop)[4],
-                                           int nvalid, int rowbase, bool isC, bool mine,
-                                           bool plain, float scale2) {
+                                           int nvalid, int rowbase, bool isC, bool plain,
+                                           float scale2) {
   f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
@@ -135,7 +136,8 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
     S.mrun = mnew;
   }
 
-  // |v|^2 of the lane's 4 rows (exact fp32 products)
+  // |v|^2 of the lane's 4 rows (exact fp32 products; the bf16 pair dot instruction is not
+  // accurate enough here: the variance moved by 2.5% with it)
   float nv2[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -165,27 +167,29 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
   // o and Cv on bf16 MFMAs (16x16x32), exactly: every fp32 weight is split into three bf16
   // terms hi + mid + lo (successive 8-bit pieces of its significand, each difference exact), and
   // V (bf16) times each term is an exact product, so only the fp32 summation rounds.  The
-  // contraction runs over this row group's 4 rows x {hi, mid} in one MFMA and 4 rows x {lo, 0}
-  // in a second, against each V element taken twice.  Lane (g, c) holds rows 4g + j at dims
-  // 8c .. 8c + 7 of V, which is the B operand for dims 8c + e, e = 0..7.
-  u32x4 whm, wlo;
+  // contraction runs over this row group's 4 rows x {hi, mid} in one MFMA (A = [hi_0 .. hi_3,
+  // mid_0 .. mid_3]) and 4 rows x {lo, 0} in a second (A = [lo_0 .. lo_3, 0 x 4]), against
+  // B = [v_0, v_1, v_2, v_3, v_0, v_1, v_2, v_3] at one dim.  Lane (g, c) holds rows 4g + j at
+  // dims 8c .. 8c + 7 of V, which is the B operand for dims 8c + e, e = 0..7.
+  uint32_t hb[4], mb[4], lb[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint32_t hb = __float_as_uint(val[i]) & 0xffff0000u;
-    const float r = val[i] - __uint_as_float(hb);  // exact: the low 16 significand bits
-    const uint32_t mb = __float_as_uint(r) & 0xffff0000u;
-    const float lo = r - __uint_as_float(mb);  // exact, and exact in bf16
-    whm[i] = (hb >> 16) | mb;
-    wlo[i] = __float_as_uint(lo) >> 16;
+    hb[i] = __float_as_uint(val[i]) & 0xffff0000u;
+    const float r = val[i] - __uint_as_float(hb[i]);  // exact: the low 16 significand bits
+    mb[i] = __float_as_uint(r) & 0xffff0000u;
+    lb[i] = __float_as_uint(r - __uint_as_float(mb[i]));  // exact, and exact in bf16
   }
+  // the high halves of two words, the first one's in the low half
+  auto hh = [](uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x07060302u); };
+  const u32x4 whm = {hh(hb[0], hb[1]), hh(hb[2], hb[3]), hh(mb[0], mb[1]), hh(mb[2], mb[3])};
+  const u32x4 wlo = {hh(lb[0], lb[1]), hh(lb[2], lb[3]), 0u, 0u};
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    u32x4 bop;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t x = T.v[j][e >> 1];
-      bop[j] = __builtin_amdgcn_perm(x, x, (e & 1) ? 0x03020302u : 0x01000100u);  // element twice
-    }
+    // element e of rows (0, 1) and of rows (2, 3), each pair in one word
+    const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+    const uint32_t p01 = __builtin_amdgcn_perm(T.v[1][e >> 1], T.v[0][e >> 1], sel);
+    const uint32_t p23 = __builtin_amdgcn_perm(T.v[3][e >> 1], T.v[2][e >> 1], sel);
+    const u32x4 bop = {p01, p23, p01, p23};
     S.acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, whm),
                                                       __builtin_bit_cast(bf16x8, bop), S.acc[e], 0,
                                                       0, 0);
@@ -194,13 +198,13 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
                                                       0, 0);
   }
 
-  // Range-term candidates: weight lanes take the rows of even tiles, variance lanes (same
-  // logits) those of odd tiles (`mine`).  Every such row is offered to the lane's sorted top-4;
-  // whatever falls off the end only raises the dropped maxima.
+  // Range-term candidates: the weight lane of a head takes rows 0 and 1 of its row group, the
+  // variance lane (same logits, so the same keys) rows 2 and 3.  Each such row is offered to the
+  // lane's sorted top-4; whatever falls off the end only raises the dropped maxima.
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float nk = mine ? kap[i] : 0.0f, ng = mine ? gsq[i] : 0.0f;
-    int nr = rowbase + i;
+  for (int i = 0; i < 2; ++i) {
+    float nk = isC ? kap[i + 2] : kap[i], ng = isC ? gsq[i + 2] : gsq[i];
+    int nr = rowbase + (isC ? i + 2 : i);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bool sw = nk > S.ck[e];
@@ -575,7 +579,8 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       const float fk = scale_of(blk[kChM], M) / hs[kHsL];
       const float bterm = blk[kChB] * hs[kHsYn];
       // only the rows of a candidate lane whose own bound still exceeds the best value: lane i
-      // kept row group i % 4 of the chunk's tiles of parity i / 4 (64 rows)
+      // kept rows 2 (i / 4) and 2 (i / 4) + 1 of row group i % 4 in every tile of the chunk
+      // (64 rows)
       const int i = lane >> 3;  // lane group i decides for candidate lane i
       const float ai = __uint_as_float(
           ((__float_as_uint(blk[kChAL + (i & 3) / 2 + 2 * (i >> 2)]) >> (16 * (i & 1))) & 0xffffu) << 16);
@@ -584,7 +589,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       for (uint64_t lm = lanes; lm; lm &= lm - 1) {
         const int li = (int)__builtin_ctzll(lm) >> 3;
         if (lane == 0) atomicAdd(L.diag + (int64_t)u * L.nhb + h0 / kHeadBlock, 1u);
-        const int j = ra + 32 * (lane >> 2) + 16 * (li >> 2) + 4 * (li & 3) + (lane & 3);
+        const int j = ra + 16 * (lane >> 1) + 4 * (li & 3) + 2 * (li >> 2) + (lane & 1);
         if (j >= rz) continue;
         const uint4 *kr = reinterpret_cast<const uint4 *>(L.Kc + (cbase + j) * kHeadDim);
         const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + j) * kHeadDim);
@@ -717,8 +722,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   constexpr int kChunkTiles = kChunkRows / 16;
   // tile tt of the split, then the flush of its chunk if tt ends one
   auto step = [&](const Tile &T, int tt) {
-    split_tile(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, isC == ((tt & 1) != 0), plain,
-               scale2);
+    split_tile(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, plain, scale2);
     if ((tt + 1) % kChunkTiles == 0)
       flush_chunk<GB>(S, s_chunk, tt / kChunkTiles, g, c, row0 + (tt / kChunkTiles) * kChunkRows);
   };
