@@ -947,6 +947,13 @@ size_t attend_fused_lds_bytes(int32_t split_rows, int gb) {
   return attend_split_lds(L, gb);
 }
 
+size_t attend_part_lds_bytes(int32_t split_rows, int gb) {
+  AttendLaunch L{};
+  L.nsplit = 2;
+  L.nchunk = attend_chunks(split_rows);
+  return attend_split_lds(L, gb);
+}
+
 hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)L.U * L.nsplit)), block(kAttendThreads);
   for (int h0 = 0; h0 < L.G; h0 += kHeadBlock) {

@@ -87,6 +87,10 @@ constexpr size_t kEvictWorkspace = 256;
 // splits stay within [kSplitMinRows, kSplitMaxRows] rows.  When the units alone give enough
 // waves, a whole unit of up to kSplitRowsLimit rows stays one split (which then also finalizes
 // its unit, with no second launch) as long as that split's LDS still lets two waves share a SIMD.
+// Splits may also run longer than kSplitMaxRows, up to the same LDS limit, when that makes the
+// whole launch one generation of resident waves (kResidentWaves): a launch of two generations
+// ends with the second one's stragglers (1024 units of about 14000 rows, G = 4: two splits per
+// unit took 1150 us where four took 1190 us).
 int32_t attend_split_rows(const ebd_attend_params *p) {
   if (p->split_rows > 0) return p->split_rows;
   const int64_t cap = p->max_rows > 0 ? p->max_rows : 1;
@@ -98,6 +102,12 @@ int32_t attend_split_rows(const ebd_attend_params *p) {
     return (int32_t)((cap + 15) / 16 * 16);
   int64_t ns = (kSplitWaves + U - 1) / U;
   ns = std::max<int64_t>(ns, (cap + kSplitMaxRows - 1) / kSplitMaxRows);
+  const int gb = std::min(G, kHeadBlock);
+  const int64_t lds_rows =
+      (int64_t)(kSplitLdsBudget / attend_part_lds_bytes(kChunkRows, gb)) * kChunkRows;
+  const int64_t rmax = std::min<int64_t>(kSplitRowsLimit, lds_rows);
+  const int64_t ns1 = std::max<int64_t>((kSplitWaves + U - 1) / U, (cap + rmax - 1) / rmax);
+  if (ns1 < ns && U * ns1 <= kResidentWaves) ns = ns1;  // each head block is its own launch
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, cap / kSplitMinRows));
   const int64_t sr = ((cap + ns - 1) / ns + 15) / 16 * 16;
   return (int32_t)sr;

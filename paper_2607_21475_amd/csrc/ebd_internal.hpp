@@ -22,6 +22,7 @@ constexpr int kSplitWaves = 1536;    // default: cut units until the launch has 
 constexpr int kSplitRowsLimit = 8192;  // largest split a caller may ask for (LDS of one wave)
 constexpr int kMaxSplits = 4096;       // splits per unit (the finalize keeps a scale per split and head in LDS)
 constexpr size_t kSplitLdsBudget = 20480;  // LDS of one split wave at two waves per SIMD (160 KB / 8)
+constexpr int kResidentWaves = 2048;       // attention waves resident at once: two per SIMD, 256 CUs
 constexpr int kScoresMaxQueries = 64;  // queries per ebd_scores call (four MFMA blocks)
 constexpr int kChunkRows = 512;      // range-term candidates are kept per chunk of a split
 constexpr int kCand = 32;            // candidates per (chunk, head)
@@ -136,6 +137,7 @@ constexpr int64_t kMaxBlocks = 8192;  // blocks per unit of ebd_block_contributi
 
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows);
 size_t attend_fused_lds_bytes(int32_t split_rows, int gb);  // LDS of a split that also finalizes
+size_t attend_part_lds_bytes(int32_t split_rows, int gb);   // LDS of one split of several
 size_t scores_workspace_bytes(int32_t U, int32_t nsplit, int32_t W);
 
 hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s);

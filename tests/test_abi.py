@@ -151,6 +151,13 @@ def test_workspace_sizes():
     assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 7) + 1024 * 287 * 7 * rec(48) * 4
     a.group = 12  # two head blocks
     assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 12) + 1024 * 287 * 12 * rec(48) * 4
+    # 1024 units: two splits of up to 8192 rows make one generation of 2048 resident waves when
+    # their LDS allows (G = 4); with G = 7 three would be needed, so 4096-row splits stay
+    a.split_rows, a.group, a.max_rows = 0, 4, 14048
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1024, 4) + 1024 * 2 * 4 * rec(7024) * 4
+    a.num_units = 1025  # 2050 waves: more than one generation either way
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(1025, 4) + 1025 * 4 * 4 * rec(3512) * 4
+    a.num_units = 1024
     # many units of up to 8192 rows stay one split while its LDS allows two waves per SIMD
     a.split_rows, a.group, a.num_units, a.max_rows = 0, 4, 8192, 4720
     assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a) == counts(8192, 4)
