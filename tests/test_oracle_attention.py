@@ -163,3 +163,70 @@ def test_empty_retained_set():
                                 np.zeros(0, np.float32))
     assert np.all(out["y"] == 0) and np.all(out["vhat"] == 0) and np.all(out["r"] == 0)
     assert np.all(np.isneginf(out["lse"]))
+
+
+def _axis_cache(rows, pis, d=128):
+    """q = 0 (every a_j = 1) and value rows given by a few leading coordinates (exact in bf16)."""
+    n = len(rows)
+    q = np.zeros((1, d), np.uint16)
+    K = np.zeros((n, d), np.uint16)
+    V = np.zeros((n, d))
+    for j, r in enumerate(rows):
+        V[j, : len(r)] = r
+    return q, K, to_bf16_bits(V), np.asarray(pis, np.float32)
+
+
+@pytest.mark.parametrize("delta", [0.1, 0.01])
+def test_radius_hand_worked_one_tail_row(delta):
+    # Rows v0 = 4 e0 and v1 = 4 e1 kept with pi = 1, v2 = 0 kept with pi = 1/2; with q = 0 every
+    # a_j = 1, so the Hajek weights a/pi are 1, 1, 2 and Nhat = 4 (eq. (3)):
+    #   yhat = (v0 + v1 + 2 v2) / 4 = (1, 1),  |yhat| = sqrt(2)
+    #   Theorem 2: Vhat = (1 - 1/2) / (1/2)^2 * 1 * |v2 - yhat|^2 / 4^2 = 2 * 2 / 16 = 1/4
+    #   eq. (4):   b = sqrt(1 - 1/2) / (1/2) * 1 * |v2 - yhat| / 4 = 1/2
+    #              r = (sqrt(2 Vhat L) + b L) / (|yhat| + eps0),  L = ln(1/delta)
+    q, K, V, pi = _axis_cache([(4.0, 0.0), (0.0, 4.0), (0.0, 0.0)], [1.0, 1.0, 0.5])
+    out = oracle.attend_certify(q, K, V, pi, delta=delta)
+    L = np.log(1.0 / delta)
+    np.testing.assert_allclose(out["y"][0, :2], [1.0, 1.0], rtol=1e-15)
+    np.testing.assert_allclose(out["vhat"][0], 0.25, rtol=1e-14)
+    np.testing.assert_allclose(out["b"][0], 0.5, rtol=1e-14)
+    r = (np.sqrt(2 * 0.25 * L) + 0.5 * L) / (np.sqrt(2.0) + 1e-9)
+    np.testing.assert_allclose(out["r"][0], r, rtol=1e-13)
+
+
+@pytest.mark.parametrize("delta", [0.1, 0.3])
+def test_radius_hand_worked_two_tail_rows(delta):
+    # v0 = 4 e0 (pi = 1), v1 = 0 and v2 = 4 e1 (pi = 1/2 each); q = 0, so a/pi = 1, 2, 2 and
+    # Nhat = 5: yhat = (4, 8) / 5 = (0.8, 1.6), |yhat|^2 = 3.2;  |v1 - yhat|^2 = 3.2 and
+    # |v2 - yhat|^2 = 0.64 + 5.76 = 6.4.  Each tail term carries (1 - pi)/pi^2 / Nhat^2 = 2/25:
+    #   Vhat = 2/25 (3.2 + 6.4) = 0.768,  b = sqrt(2/25 * 6.4) = sqrt(0.512)  (the larger term)
+    q, K, V, pi = _axis_cache([(4.0, 0.0), (0.0, 0.0), (0.0, 4.0)], [1.0, 0.5, 0.5])
+    out = oracle.attend_certify(q, K, V, pi, delta=delta)
+    L = np.log(1.0 / delta)
+    np.testing.assert_allclose(out["y"][0, :2], [0.8, 1.6], rtol=1e-15)
+    np.testing.assert_allclose(out["vhat"][0], 0.768, rtol=1e-14)
+    np.testing.assert_allclose(out["b"][0], np.sqrt(0.512), rtol=1e-14)
+    r = (np.sqrt(2 * 0.768 * L) + np.sqrt(0.512) * L) / (np.sqrt(3.2) + 1e-9)
+    np.testing.assert_allclose(out["r"][0], r, rtol=1e-13)
+
+
+@pytest.mark.parametrize("delta", [0.1, 0.05])
+def test_radius_single_tail_row_closed_form(delta):
+    # One retained tail row j: its Hajek weight w_j = (a_j / pi_j) / Nhat is the softmax of the
+    # offset logits s - ln pi (torch, fp64), Theorem 2 has the single term (1 - pi_j) w_j^2
+    # |v_j - yhat|^2 and the range term is its square root, so eq. (4) reduces to
+    #   r = b (sqrt(2 L) + L) / (|yhat| + eps0),  b = sqrt(1 - pi_j) w_j |v_j - yhat|.
+    q, K, V, pi = _case(11, G=3, n=64)
+    pi[:] = 1.0
+    j = 41
+    pi[j] = 0.07
+    out = oracle.attend_certify(q, K, V, pi, delta=delta)
+    s = bf16_to_f64(q) @ bf16_to_f64(K).T / np.sqrt(128) - np.log(pi.astype(np.float64))
+    w = torch.softmax(torch.tensor(s), dim=1).numpy()
+    y = w @ bf16_to_f64(V)
+    b = np.sqrt(1 - np.float64(pi[j])) * w[:, j] * np.linalg.norm(bf16_to_f64(V)[j] - y, axis=1)
+    L = np.log(1.0 / delta)
+    np.testing.assert_allclose(out["b"], b, rtol=1e-12)
+    np.testing.assert_allclose(out["vhat"], b ** 2, rtol=1e-12)
+    r = b * (np.sqrt(2 * L) + L) / (np.linalg.norm(y, axis=1) + 1e-9)
+    np.testing.assert_allclose(out["r"], r, rtol=1e-12)

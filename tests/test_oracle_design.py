@@ -145,12 +145,12 @@ def _replicate(q, K, V, pi, R, seed, delta=0.1):
     return ev, at
 
 
-def test_monte_carlo_matches_enumeration():
+@pytest.mark.parametrize("R", [20000, pytest.param(100000, marks=pytest.mark.slow)])
+def test_monte_carlo_matches_enumeration(R):
     q, K, V, pi = tiny_cache(3, shift=-2.0)
     E = enumerate_design(q, K, V, pi, 4)
     M = _oracle_moments(q, K, V, pi, E)
-    R = 20000
-    ev, at = _replicate(q, K, V, pi, R, seed=4242)
+    ev, at = _replicate(q, K, V, pi, R, seed=4242 + R)
     # the draws are the Poisson design: mean retained tail size
     np.testing.assert_allclose(ev["count"].mean() - 4, pi[4:].astype(np.float64).sum(),
                                atol=5 * np.sqrt((pi[4:] * (1 - pi[4:].astype(np.float64))).sum() / R))
