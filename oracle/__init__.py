@@ -73,7 +73,7 @@ def _load():
     lib.ebd_ref_full_attention.argtypes = [i32, i32, i64, P, P, P, f64, P]
     lib.ebd_ref_full_attention.restype = None
     lib.ebd_ref_evict_batch.argtypes = [i32, i32, P, P, P, P, P, i32, i32, f64, P, f64, u64, P, u32,
-                                        i32, i32, P, P, P, P, P, P, P, P, P, i32]
+                                        i32, i32, P, P, P, P, P, P, P, P, P, P, i32]
     lib.ebd_ref_systematic_start.argtypes = [u64, u32, u32]
     lib.ebd_ref_systematic_start.restype = u32
     lib.ebd_ref_mask_systematic.argtypes = [i64, P, u64, u32, u32, P]
@@ -230,7 +230,7 @@ def full_attention(q, K, V, scale=None):
 # --------------------------------------------------------------------------
 def evict_batch(seq_off, cap_off, scores, K, V, n_sink, n_recent, budget_frac=0.1,
                 budget_per_unit=None, pi_min=0.01, seed=0, seed_per_unit=None, epoch=0,
-                pi_mode=0, pi_given=None, design=0, nthreads=0):
+                pi_mode=0, pi_given=None, design=0, nthreads=0, unit_ids=None):
     seq_off = _c(seq_off, np.int64)
     cap_off = _c(cap_off, np.int64)
     U = seq_off.shape[0] - 1
@@ -243,6 +243,7 @@ def evict_batch(seq_off, cap_off, scores, K, V, n_sink, n_recent, budget_frac=0.
     bpu = None if budget_per_unit is None else _c(budget_per_unit, np.float32)
     spu = None if seed_per_unit is None else _c(seed_per_unit, np.uint64)
     pg = None if pi_given is None else _c(pi_given, np.float32)
+    uid = None if unit_ids is None else _c(unit_ids, np.uint32)
     out = {
         "Kc": np.zeros((max(crow, 1), d), np.uint16),
         "Vc": np.zeros((max(crow, 1), d), np.uint16),
@@ -255,7 +256,8 @@ def evict_batch(seq_off, cap_off, scores, K, V, n_sink, n_recent, budget_frac=0.
     }
     _load().ebd_ref_evict_batch(U, d, _p(seq_off), _p(cap_off), _p(scores), _p(K), _p(V), n_sink,
                                 n_recent, float(budget_frac), _p(bpu), float(pi_min), int(seed),
-                                _p(spu), int(epoch), int(pi_mode), int(design), _p(pg), _p(out["Kc"]),
+                                _p(spu), int(epoch), int(pi_mode), int(design), _p(pg), _p(uid),
+                                _p(out["Kc"]),
                                 _p(out["Vc"]), _p(out["pic"]), _p(out["idx"]), _p(out["count"]),
                                 _p(out["lambda"]), _p(out["pi_full"]), _p(out["status"]),
                                 int(nthreads))

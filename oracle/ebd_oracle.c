@@ -604,13 +604,15 @@ void ebd_ref_window_scores(int64_t n, int32_t d, int32_t W, const uint16_t *K, c
  *   pi_full [rows] (optional) receives the fp32 pi of every position.
  *   pi_given [rows] (optional): use these fp32 pi instead of solving (parity of
  *   the mask and compaction given the same pi).
+ *   unit_ids [U] (optional): the unit word of each unit's Philox counter (default u), so that
+ *   a sample of units drawn from a larger batch gets the same streams as in that batch.
  */
 void ebd_ref_evict_batch(int32_t U, int32_t d, const int64_t *seq_off, const int64_t *cap_off,
                          const float *scores, const uint16_t *K, const uint16_t *V,
                          int32_t n_sink, int32_t n_recent, double budget_frac,
                          const float *budget_per_unit, double pi_min, uint64_t seed,
                          const uint64_t *seed_per_unit, uint32_t epoch, int32_t pi_mode,
-                         int32_t design, const float *pi_given,
+                         int32_t design, const float *pi_given, const uint32_t *unit_ids,
                          uint16_t *Kc, uint16_t *Vc, float *pic, int32_t *idxc, int32_t *count,
                          double *lambda_out, float *pi_full, uint32_t *status, int32_t nthreads)
 {
@@ -645,10 +647,11 @@ void ebd_ref_evict_batch(int32_t U, int32_t d, const int64_t *seq_off, const int
             for (int64_t i = 0; i < n; ++i) pi32[i] = (float)pi64[i];
         }
         uint64_t sd = seed_per_unit ? seed_per_unit[u] : seed;
+        uint32_t uid = unit_ids ? unit_ids[u] : (uint32_t)u;
         if (design == REF_DESIGN_SYSTEMATIC)
-            ebd_ref_mask_systematic(n, pi32, sd, (uint32_t)u, epoch, mask);
+            ebd_ref_mask_systematic(n, pi32, sd, uid, epoch, mask);
         else
-            ebd_ref_mask(n, pi32, sd, (uint32_t)u, epoch, mask);
+            ebd_ref_mask(n, pi32, sd, uid, epoch, mask);
         int64_t kept = ebd_ref_compact(n, d, mask, pi32, K + base * d, V + base * d, cap,
                                        Kc + cbase * d, Vc + cbase * d, pic + cbase, idxc + cbase);
         if (kept > cap) st |= REF_ST_CAP_OVERFLOW;

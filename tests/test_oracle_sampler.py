@@ -265,3 +265,28 @@ def test_evict_batch_ragged_units():
         c0 = coff[u]
         np.testing.assert_array_equal(out["idx"][c0:c0 + len(keep)], keep)
         np.testing.assert_array_equal(out["Kc"][c0:c0 + len(keep)], K[off[u] + keep])
+
+
+def test_evict_batch_unit_ids_select_the_stream():
+    """A sample of units evicted on its own, with the units' ids in the larger batch as the Philox
+    unit word, retains exactly what the whole batch retains for those units."""
+    rng = np.random.default_rng(5)
+    lens = [500] * 9
+    d = 8
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    K = rng.integers(0, 1 << 16, (int(off[-1]), d), dtype=np.uint16)
+    V = rng.integers(0, 1 << 16, (int(off[-1]), d), dtype=np.uint16)
+    s = _heavy_scores(int(off[-1]), 3)
+    full = oracle.evict_batch(off, off, s, K, V, 4, 16, budget_frac=0.3, seed=5)
+    pick = np.array([7, 2, 5], np.int64)
+    rows = np.concatenate([np.arange(off[u], off[u + 1]) for u in pick])
+    soff = np.arange(len(pick) + 1, dtype=np.int64) * 500
+    sub = oracle.evict_batch(soff, soff, s[rows], K[rows], V[rows], 4, 16, budget_frac=0.3, seed=5,
+                             unit_ids=pick.astype(np.uint32))
+    plain = oracle.evict_batch(soff, soff, s[rows], K[rows], V[rows], 4, 16, budget_frac=0.3, seed=5)
+    for i, u in enumerate(pick):
+        c = full["count"][u]
+        assert sub["count"][i] == c
+        np.testing.assert_array_equal(sub["idx"][soff[i]:soff[i] + c], full["idx"][off[u]:off[u] + c])
+    assert not np.array_equal(plain["count"], sub["count"]) or not np.array_equal(
+        plain["idx"], sub["idx"])  # local ids draw other streams
