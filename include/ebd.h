@@ -42,7 +42,8 @@ typedef enum ebd_status {
     EBD_ERR_HIP = 4          /* a HIP runtime call failed (launch, event) */
 } ebd_status;
 
-/* Per-unit status bits written by ebd_evict (status[u]) and ebd_append_certain. */
+/* Per-unit status bits written by ebd_evict (status[u]), ebd_append_certain and
+   ebd_attend_certify. */
 #define EBD_ST_CAP_OVERFLOW 1u /* retained count exceeds the unit's capacity: rows at or
                                   beyond the capacity are NOT written; count[u] holds the
                                   true count; re-run with a larger capacity */
@@ -52,8 +53,10 @@ typedef enum ebd_status {
                                   of them get pi = 1 (zero scores keep pi_min) */
 #define EBD_ST_BAD_SCORE 8u    /* a NaN, infinite or negative score was seen; it is
                                   treated as 0 (pi = pi_min) */
-#define EBD_ST_BAD_LAYOUT 16u  /* the unit exceeds params.max_rows or params.max_capacity:
-                                  nothing was sampled or written for it and count[u] = 0 */
+#define EBD_ST_BAD_LAYOUT 16u  /* ebd_evict: the unit exceeds params.max_rows or
+                                  params.max_capacity: nothing was sampled or written for it
+                                  and count[u] = 0.  ebd_attend_certify: the unit holds more
+                                  rows than params.max_rows; those past it were not seen */
 
 /*
  * Sampler parameters (Sec. 3.3, eq. (2) and the certainty set).
@@ -138,11 +141,12 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
  * Certified decode attention parameters (Sec. 3.3 eq. (3), Theorem 2; Sec. 3.4 eq. (4)).
  *   group G: query heads per KV head (q is [U, G, 128]); any G >= 1.
  *   cap_off [U+1] device int64: the compacted layout written by ebd_evict.
- *   max_rows host value >= max_u (cap_off[u+1] - cap_off[u]); sizes the split grid.
+ *   max_rows host value >= the most rows any unit holds; sizes the split grid (rows of a unit
+ *   beyond it are not seen, and flagged in the status words).
  *   scale: logit scale (0 means 1/sqrt(head_dim)); delta (0 means 0.1) and eps0
  *   (0 means 1e-9): the confidence level and normaliser of eq. (4).
  *   split_rows: retained rows per split, one wave each (0 = library choice; else a
- *   multiple of 16 in [16, 8192]).  Retained rows of a unit beyond max_rows are ignored.
+ *   multiple of 16 in [16, 8192]).
  *   A unit spans at most 4096 splits: max_rows above 4096 split rows (with the library's
  *   choice, above 4096 x 4096 rows) returns EBD_ERR_UNSUPPORTED.
  *   flags: 0, or EBD_F_NO_OFFSET: y and ln N are those of the uncorrected retained softmax
@@ -167,24 +171,33 @@ typedef struct ebd_attend_params {
 
 /*
  * ebd_attend_certify -- one decode step of certified attention over the retained rows.
- *   q [U, G, 128] bf16; Kc, Vc, pic, count as written by ebd_evict (rows beyond
- *   min(count[u], capacity) are ignored).
+ *   q [U, G, 128] bf16; Kc, Vc, pic, count as written by ebd_evict.  The step sees the first
+ *   min(count[u], capacity, max_rows) rows of unit u; what it cannot see is reported in status.
  *   Outputs per (unit, query head), fp32:
  *     y      [U, G, 128]  Hajek output yhat = sum_S (a/pi) v / sum_S (a/pi)      (eq. (3))
  *     vhat   [U, G]       variance estimate of Theorem 2
  *     lse    [U, G]       ln Nhat, Nhat = sum_S a/pi (a = exp(scale q.k)); -inf if S empty
  *     brange [U, G]       range term b of eq. (4) (exact maximum), or NULL
  *     radius [U, G]       radius r of eq. (4), or NULL
+ *     status [U] uint32 or NULL, written (not or-ed): EBD_ST_CAP_OVERFLOW when count[u] exceeds
+ *            the unit's capacity (rows past the capacity were never stored and are not seen),
+ *            EBD_ST_BAD_LAYOUT when the unit holds more rows than max_rows (the rows past
+ *            max_rows are not seen); 0 otherwise.  The outputs then cover the rows seen.
+ *   vhat is accumulated in the same pass as C2 - 2 yhat.Cv + |yhat|^2 C0 (C0 = sum c,
+ *   Cv = sum c v, C2 = sum c |v|^2, c = (1 - pi) (a/pi)^2); a head where these terms cancel
+ *   (one tail row dominating both yhat and the variance) is summed again directly over the
+ *   unit's rows, sum c |v - yhat|^2, in the same call.
  *   workspace: at least ebd_workspace_size(EBD_WS_ATTEND, p) bytes, 256-byte aligned; y must
- *   be 16-byte aligned.  After the call the workspace starts with U * ceil(G / 8) uint32
- *   counts, per (unit, block of 8 query heads): the 512-row chunks re-read to make the range
- *   term exact (0 when the kept candidates already decide it).  When every unit fits one
- *   split, the whole step is one kernel and the workspace holds only these counts.
+ *   be 16-byte aligned.  After the call the workspace starts with two uint32 counts per (unit,
+ *   block of 8 query heads): the 512-row chunks re-read to make the range term exact (0 when
+ *   the kept candidates already decide it), then the heads whose vhat was summed directly.
+ *   When every unit fits one split, the whole step is one kernel and the workspace holds only
+ *   these counts.
  */
 ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
                               const uint16_t *Vc, const float *pic, const int32_t *count,
                               float *y, float *vhat, float *lse, float *brange, float *radius,
-                              void *workspace, size_t ws_bytes, void *stream);
+                              uint32_t *status, void *workspace, size_t ws_bytes, void *stream);
 
 /*
  * ebd_append_certain -- append one decode token per unit to its retained set with pi = 1
@@ -248,7 +261,7 @@ ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint1
  *   y, lse: the outputs of ebd_attend_certify for the same q (yhat and ln Nhat).
  *   Rows with pi = 1, with idxc < 0 (appended decode rows) or past the last block add nothing.
  *   block_rows >= 1; 1 <= nblocks <= 8192; max_rows as for ebd_attend_certify (rows of a unit
- *   beyond it are ignored), at most 2^24 (else EBD_ERR_UNSUPPORTED).  blocks [U, nblocks] fp32
+ *   beyond it are ignored), below 2^24 (else EBD_ERR_UNSUPPORTED).  blocks [U, nblocks] fp32
  *   is written.  No workspace.
  */
 typedef struct ebd_blocks_params {
@@ -310,13 +323,14 @@ const char *ebd_status_string(ebd_status s);
 const char *ebd_version(void);
 
 /*
- * Kernel timing (profiling aid).  While enabled, every kernel launch of the library is
- * bracketed by HIP events recorded on the launch stream.  ebd_timing_read() waits for the
- * recorded events, and adds the elapsed times of kernel `name` ("evict_select",
- * "evict_copy", "attend_split", "attend_finalize", "append_certain", "scores_stats",
- * "scores_accum", "block_contrib", "cert_step") to *total_ms and
- * its launch count to *launches; it then clears that kernel's record.  Not meant for use
- * from several host threads at once.
+ * Kernel timing (a process-wide profiling aid, off by default).  While enabled, every kernel
+ * launch of the library is bracketed by HIP events recorded on its own launch stream.
+ * ebd_timing_read() waits for the recorded events, and adds the elapsed times of kernel `name`
+ * ("evict_select", "evict_copy", "attend_split", "attend_finalize", "append_certain",
+ * "scores_stats", "scores_accum", "block_contrib", "cert_step") to *total_ms and its launch
+ * count to *launches; it then clears that kernel's record.  The switch is an atomic flag and the
+ * records are guarded by a lock, so both calls may come from any host thread; while timing is
+ * off no event is created and launches take no lock.
  */
 ebd_status ebd_timing_enable(int32_t enable);
 ebd_status ebd_timing_read(const char *name, double *total_ms, int64_t *launches);

@@ -131,7 +131,7 @@ class ebd_cert_params(ctypes.Structure):
 _P = ctypes.c_void_p
 _lib.ebd_evict.argtypes = [ctypes.POINTER(ebd_evict_params)] + [_P] * 12 + [ctypes.c_size_t, _P]
 _lib.ebd_evict.restype = ctypes.c_int
-_lib.ebd_attend_certify.argtypes = [ctypes.POINTER(ebd_attend_params)] + [_P] * 11 + \
+_lib.ebd_attend_certify.argtypes = [ctypes.POINTER(ebd_attend_params)] + [_P] * 12 + \
     [ctypes.c_size_t, _P]
 _lib.ebd_attend_certify.restype = ctypes.c_int
 _lib.ebd_scores.argtypes = [ctypes.POINTER(ebd_scores_params)] + [_P] * 4 + [ctypes.c_size_t, _P]
@@ -271,7 +271,7 @@ def ebd_evict(params: ebd_evict_params, scores, K, V, Kc, Vc, pic, idxc, count, 
 
 
 def ebd_attend_certify(params: ebd_attend_params, q, Kc, Vc, pic, count, y, vhat, lse, workspace,
-                       brange=None, radius=None, stream=None) -> None:
+                       brange=None, radius=None, status=None, stream=None) -> None:
     """Launch certified decode attention (asynchronous on the current stream)."""
     bf = torch.bfloat16
     f32 = torch.float32
@@ -280,6 +280,7 @@ def ebd_attend_certify(params: ebd_attend_params, q, Kc, Vc, pic, count, y, vhat
                                    _ptr(count, torch.int32, "count"), _ptr(y, f32, "y"),
                                    _ptr(vhat, f32, "vhat"), _ptr(lse, f32, "lse"),
                                    _ptr(brange, f32, "brange"), _ptr(radius, f32, "radius"),
+                                   _ptr(status, torch.int32, "status"),
                                    _ptr(workspace, None, "workspace"),
                                    workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ebd_attend_certify", code)

@@ -118,9 +118,10 @@ def attend_certify(cache: RetainedCache, q: torch.Tensor, split_rows: int = 0, d
     lse = torch.empty((U, G), dtype=torch.float32, device=dev)
     b = torch.empty((U, G), dtype=torch.float32, device=dev)
     r = torch.empty((U, G), dtype=torch.float32, device=dev)
+    st = torch.empty((U,), dtype=torch.int32, device=dev)
     ebd_attend_certify(p, q, cache.Kc, cache.Vc, cache.pic, cache.count, y, vhat, lse, ws,
-                       brange=b, radius=r)
-    return {"y": y, "vhat": vhat, "lse": lse, "b": b, "r": r, "ws": ws}
+                       brange=b, radius=r, status=st)
+    return {"y": y, "vhat": vhat, "lse": lse, "b": b, "r": r, "status": st, "ws": ws}
 
 
 def importance_scores(K: torch.Tensor, seq_off: torch.Tensor, q: torch.Tensor, max_rows: int,
@@ -141,15 +142,25 @@ def importance_scores(K: torch.Tensor, seq_off: torch.Tensor, q: torch.Tensor, m
     return scores, ws
 
 
+def _diag(ws: torch.Tensor, num_units: int, group: int) -> torch.Tensor:
+    nhb = (int(group) + 7) // 8
+    return ws[: 8 * num_units * nhb].view(torch.int32).view(num_units * nhb, 2)
+
+
 def rescans(ws: torch.Tensor, num_units: int, group: int) -> int:
     """512-row chunks the last ebd_attend_certify on `ws` rescanned for the exact range term
-    (the workspace starts with one count per unit and block of 8 query heads)."""
-    nhb = (int(group) + 7) // 8
-    return int(ws[: 4 * num_units * nhb].view(torch.int32).sum().item())
+    (the workspace starts with two counts per unit and block of 8 query heads)."""
+    return int(_diag(ws, num_units, group)[:, 0].sum().item())
+
+
+def direct_variances(ws: torch.Tensor, num_units: int, group: int) -> int:
+    """Query heads whose Vhat the last ebd_attend_certify on `ws` summed directly because the
+    one-pass expansion cancelled."""
+    return int(_diag(ws, num_units, group)[:, 1].sum().item())
 
 
 def fused_finalize(ws_bytes: int, num_units: int, group: int) -> bool:
     """Whether an attention launch planned with this workspace size finalizes inside its split
-    kernel (every unit is one split: the workspace holds only the rescan counts)."""
+    kernel (every unit is one split: the workspace holds only the diagnostic counts)."""
     nhb = (int(group) + 7) // 8
-    return ws_bytes <= (4 * num_units * nhb + 255) // 256 * 256
+    return ws_bytes <= (8 * num_units * nhb + 255) // 256 * 256

@@ -31,7 +31,9 @@
 //   attend_finalize (one wave per (unit, head block)), which combines the split records by
 //   log-sum-exp.  Candidates are bounded a chunk block at a time; only those whose bound can
 //   still win are re-read, and a chunk is rescanned only if its non-candidate bound cannot
-//   exclude a larger term.
+//   exclude a larger term.  Where C2 - 2 yhat.Cv + |yhat|^2 C0 has cancelled (one tail row
+//   dominates both yhat and the variance, so yhat ~ v of that row), Vhat of that head is summed
+//   again directly, sum (1 - pi) w^2 |v - yhat|^2 over the unit's retained rows.
 #include "ebd.h"
 #include "ebd_device.hpp"
 #include "ebd_internal.hpp"
@@ -282,8 +284,18 @@ __device__ __forceinline__ void flush_chunk(SplitState &S, float *s_chunk, int k
 // the radius r, from the combined sums in LDS and the candidate blocks of every chunk.
 // ---------------------------------------------------------------------------------------------
 constexpr int kListCap = 256;  // candidates evaluated per batch
-constexpr int kHs = 8;         // per-head table: M, l, C0, C2, |yhat|, lb, Vhat, -
-constexpr int kHsM = 0, kHsL = 1, kHsC0 = 2, kHsC2 = 3, kHsYn = 4, kHsLb = 5, kHsV = 6;
+constexpr int kHs = 8;         // per-head table: M, l, C0, C2, |yhat|, lb, Vhat, redo
+constexpr int kHsM = 0, kHsL = 1, kHsC0 = 2, kHsC2 = 3, kHsYn = 4, kHsLb = 5, kHsV = 6, kHsRedo = 7;
+// The one-pass form C2 - 2 yhat.Cv + |yhat|^2 C0 of sum c |v - yhat|^2 carries a rounding error of
+// a few ulps of (sqrt(C2) + |yhat| sqrt(C0))^2 (each sum is of exact products, rounded in fp32);
+// below this fraction of that scale the head's Vhat is summed again directly.
+constexpr float kCancelFrac = 1.0f / 64.0f;
+
+// Per (unit, head block) diagnostic words at the start of the workspace: the 512-row chunks
+// rescanned for the range term, and the heads whose Vhat was summed directly.
+__device__ __forceinline__ uint32_t *diag_of(const AttendLaunch &L, int u, int h0) {
+  return L.diag + 2 * ((int64_t)u * L.nhb + h0 / kHeadBlock);
+}
 
 // LDS of the finalize, carved from one dynamic buffer.
 template <int GB>
@@ -349,17 +361,40 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     if (h < GB && j == 0) {
       float *hs = F.hs + h * kHs;
       const float l = hs[kHsL];
-      const float V = fmaxf(hs[kHsC2] - 2.0f * ycv + yy * hs[kHsC0], 0.0f) / (l * l);
-      if (!L.plain) L.vhat[uh0 + h] = V;
+      const float num = hs[kHsC2] - 2.0f * ycv + yy * hs[kHsC0];
+      const float sc = sqrtf(hs[kHsC2]) + sqrtf(yy * hs[kHsC0]);
+      const bool redo = num < kCancelFrac * sc * sc;  // never when there is no tail row (sc = 0)
+      const float V = fmaxf(num, 0.0f) / (l * l);
+      if (!L.plain && !redo) L.vhat[uh0 + h] = V;
       L.lse[uh0 + h] = hs[kHsM] * kLn2 + logf(l);
       hs[kHsYn] = sqrtf(yy);
       hs[kHsLb] = 0.0f;
       hs[kHsV] = V;
+      hs[kHsRedo] = redo ? 1.0f : 0.0f;
       F.best[h] = 0ull;
     }
   }
   __syncthreads();
   if (L.plain) return;  // the uncorrected pass only replaces y and ln N
+
+  // q of every head into the Cv slots, once Cv is no longer needed (the direct variance sums and
+  // the range-term rescans recompute logits).
+  bool qloaded = false;
+  auto load_q = [&]() {
+    if (qloaded) return;
+    for (int e = lane; e < GB * kHeadDim / 2; e += 64) {
+      const int h = e / (kHeadDim / 2), d2 = e % (kHeadDim / 2);
+      const uint32_t qw = reinterpret_cast<const uint32_t *>(L.q + (uh0 + h) * kHeadDim)[d2];
+      F.o[(GB + h) * kHeadDim + 2 * d2] = bf16_lo(qw);
+      F.o[(GB + h) * kHeadDim + 2 * d2 + 1] = bf16_hi(qw);
+    }
+    __syncthreads();
+    qloaded = true;
+  };
+
+  uint32_t redo = 0u;
+#pragma unroll
+  for (int h = 0; h < GB; ++h) redo |= (F.hs[h * kHs + kHsRedo] != 0.0f ? 1u : 0u) << h;
 
   // (2) Candidate bounds: a candidate's value f g |v - yhat| / l is at most f g (Vmax + |yhat|)/l.
   //     Candidate e = ((s nchunk + k) GB + h) kCand + j.
@@ -541,7 +576,6 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
   // (5) A chunk whose non-candidate bound f (A + B |yhat|) / l still exceeds the best value is
   //     rescanned row by row.
   const float scale2 = L.scale * kLog2e;
-  bool qloaded = false;
   for (int x0 = 0; x0 < nx; x0 += 64) {
     const int x = x0 + lane;  // (s nchunk + k) GB + h
     bool need = false;
@@ -555,16 +589,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       }
     }
     uint64_t m = __ballot(need);
-    if (m && !qloaded) {  // q of every head into the Cv slots (no longer needed)
-      for (int e = lane; e < GB * kHeadDim / 2; e += 64) {
-        const int h = e / (kHeadDim / 2), d2 = e % (kHeadDim / 2);
-        const uint32_t qw = reinterpret_cast<const uint32_t *>(L.q + (uh0 + h) * kHeadDim)[d2];
-        F.o[(GB + h) * kHeadDim + 2 * d2] = bf16_lo(qw);
-        F.o[(GB + h) * kHeadDim + 2 * d2 + 1] = bf16_hi(qw);
-      }
-      __syncthreads();
-      qloaded = true;
-    }
+    if (m) load_q();
     while (m) {
       const int xx = x0 + (int)__builtin_ctzll(m);
       m &= m - 1;
@@ -588,7 +613,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       float best = 0.0f;
       for (uint64_t lm = lanes; lm; lm &= lm - 1) {
         const int li = (int)__builtin_ctzll(lm) >> 3;
-        if (lane == 0) atomicAdd(L.diag + (int64_t)u * L.nhb + h0 / kHeadBlock, 1u);
+        if (lane == 0) atomicAdd(diag_of(L, u, h0), 1u);
         const int j = ra + 16 * (lane >> 1) + 4 * (li & 3) + 2 * (li >> 2) + (lane & 1);
         if (j >= rz) continue;
         const uint4 *kr = reinterpret_cast<const uint4 *>(L.Kc + (cbase + j) * kHeadDim);
@@ -628,6 +653,172 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     }
   }
 
+  // (5b) Heads whose one-pass variance cancelled (step (1)): Vhat and b again, directly over the
+  //      unit's retained rows and about the reference point c0 = yhat (fp32) in LDS.  One row
+  //      then dominates yhat, and yhat - c0 is of the order of c0's own rounding, so the pass
+  //      accumulates l' = sum w, o' = sum w (v - c0), C0 = sum c, Cv' = sum c (v - c0) and
+  //      S1 = sum c |v - c0|^2 (v - c0 is exact near the dominating row), then
+  //        delta = o' / l',   Vhat l'^2 = S1 - 2 delta.Cv' + |delta|^2 C0
+  //      (none of these terms cancels), and a second pass takes b exactly as
+  //      max sqrt(1 - pi) w |(v - c0) - delta| / l'.  Heads go in groups of four; 16 lanes per
+  //      row, 8 dims per lane, four rows per lane in flight.
+  if (redo) {
+    load_q();
+    const int rq = lane >> 4, c = lane & 15;
+    const float scale2d = L.scale * kLog2e;
+    for (int hg = 0; hg < GB; hg += 4) {
+      if (!((redo >> hg) & 0xfu)) continue;
+      bool act[4];
+      float q8[4][8], c8[4][8], Mh[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int h = hg + k;
+        act[k] = h < GB && ((redo >> h) & 1u);
+        const float *qs = F.o + (GB + (act[k] ? h : 0)) * kHeadDim + 8 * c;
+        const float *cs = F.o + (act[k] ? h : 0) * kHeadDim + 8 * c;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          q8[k][e] = qs[e];
+          c8[k][e] = cs[e];
+        }
+        Mh[k] = F.hs[(act[k] ? h : 0) * kHs + kHsM];
+      }
+      // Rows of a step: lane group rq takes rows j0 + 4 i + rq.  Rows past cnt get w = 0.
+      constexpr int kIn = 4;
+      auto load_rows = [&](int j0, uint4 (&kw)[kIn], uint4 (&vw)[kIn], float (&pj)[kIn],
+                           bool (&ok)[kIn]) {
+#pragma unroll
+        for (int i = 0; i < kIn; ++i) {
+          const int j = j0 + 4 * i + rq;
+          ok[i] = j < cnt;
+          kw[i] = ok[i] ? reinterpret_cast<const uint4 *>(L.Kc + (cbase + j) * kHeadDim)[c]
+                        : make_uint4(0u, 0u, 0u, 0u);
+          vw[i] = ok[i] ? reinterpret_cast<const uint4 *>(L.Vc + (cbase + j) * kHeadDim)[c]
+                        : make_uint4(0u, 0u, 0u, 0u);
+          pj[i] = ok[i] ? L.pic[cbase + j] : 1.0f;
+        }
+      };
+      // logit weight w of one row for head slot k (every lane of the row gets it)
+      auto weight = [&](int k, const uint4 &kw, float p, bool ok) -> float {
+        const uint32_t kk[4] = {kw.x, kw.y, kw.z, kw.w};
+        float dot = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          dot = fmaf(q8[k][2 * t], bf16_lo(kk[t]), dot);
+          dot = fmaf(q8[k][2 * t + 1], bf16_hi(kk[t]), dot);
+        }
+        dot = row16_sum(dot);
+        return ok ? fast_exp2(fmaf(dot, scale2d, -fast_log2(p)) - Mh[k]) : 0.0f;
+      };
+      // pass 1: the sums about c0
+      float op[4][8], cv[4][8], lp[4], c0s[4], s1[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        lp[k] = c0s[k] = s1[k] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) op[k][e] = cv[k][e] = 0.0f;
+      }
+      for (int j0 = 0; j0 < cnt; j0 += 4 * kIn) {
+        uint4 kw[kIn], vw[kIn];
+        float pj[kIn];
+        bool ok[kIn];
+        load_rows(j0, kw, vw, pj, ok);
+#pragma unroll
+        for (int i = 0; i < kIn; ++i) {
+          const uint32_t vv[4] = {vw[i].x, vw[i].y, vw[i].z, vw[i].w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (!act[k]) continue;
+            const float w = weight(k, kw[i], pj[i], ok[i]);
+            const float cc = (1.0f - pj[i]) * w * w;
+            float n2 = 0.0f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const float d0 = bf16_lo(vv[t]) - c8[k][2 * t], d1 = bf16_hi(vv[t]) - c8[k][2 * t + 1];
+              op[k][2 * t] = fmaf(w, d0, op[k][2 * t]);
+              op[k][2 * t + 1] = fmaf(w, d1, op[k][2 * t + 1]);
+              cv[k][2 * t] = fmaf(cc, d0, cv[k][2 * t]);
+              cv[k][2 * t + 1] = fmaf(cc, d1, cv[k][2 * t + 1]);
+              n2 = fmaf(d0, d0, n2);
+              n2 = fmaf(d1, d1, n2);
+            }
+            n2 = row16_sum(n2);
+            lp[k] += w;
+            c0s[k] += cc;
+            s1[k] = fmaf(cc, n2, s1[k]);
+          }
+        }
+      }
+      // combine the four row groups: vectors by lane exchange (every lane then holds the sums of
+      // its 8 dims), scalars from one lane per row group
+      float lt[4], vt[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!act[k]) continue;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          op[k][e] += __shfl_xor(op[k][e], 16);
+          op[k][e] += __shfl_xor(op[k][e], 32);
+          cv[k][e] += __shfl_xor(cv[k][e], 16);
+          cv[k][e] += __shfl_xor(cv[k][e], 32);
+        }
+        lt[k] = wave_sum(c == 0 ? lp[k] : 0.0f);
+        const float c0t = wave_sum(c == 0 ? c0s[k] : 0.0f);
+        const float s1t = wave_sum(c == 0 ? s1[k] : 0.0f);
+        float dcv = 0.0f, dd = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          op[k][e] /= lt[k];  // delta, dims 8c .. 8c + 7
+          dcv = fmaf(op[k][e], cv[k][e], dcv);
+          dd = fmaf(op[k][e], op[k][e], dd);
+        }
+        dcv = row16_sum(dcv);  // every row group holds all 128 dims: one row's lanes suffice
+        dd = row16_sum(dd);
+        vt[k] = fmaxf(s1t - 2.0f * dcv + dd * c0t, 0.0f) / (lt[k] * lt[k]);
+      }
+      // pass 2: the range term with delta known
+      float bm[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int j0 = 0; j0 < cnt; j0 += 4 * kIn) {
+        uint4 kw[kIn], vw[kIn];
+        float pj[kIn];
+        bool ok[kIn];
+        load_rows(j0, kw, vw, pj, ok);
+#pragma unroll
+        for (int i = 0; i < kIn; ++i) {
+          const uint32_t vv[4] = {vw[i].x, vw[i].y, vw[i].z, vw[i].w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (!act[k]) continue;
+            const float w = weight(k, kw[i], pj[i], ok[i]);
+            float n2 = 0.0f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const float d0 = (bf16_lo(vv[t]) - c8[k][2 * t]) - op[k][2 * t];
+              const float d1 = (bf16_hi(vv[t]) - c8[k][2 * t + 1]) - op[k][2 * t + 1];
+              n2 = fmaf(d0, d0, n2);
+              n2 = fmaf(d1, d1, n2);
+            }
+            n2 = row16_sum(n2);
+            bm[k] = fmaxf(bm[k], sqrtf(1.0f - pj[i]) * w * sqrtf(n2));
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!act[k]) continue;
+        const float b = wave_max(bm[k]) / lt[k];
+        if (lane == 0) {
+          float *hs = F.hs + (hg + k) * kHs;
+          hs[kHsV] = vt[k];
+          hs[kHsLb] = b;
+          L.vhat[uh0 + hg + k] = vt[k];
+        }
+      }
+    }
+    if (lane == 0) diag_of(L, u, h0)[1] = (uint32_t)__popc(redo);
+    __syncthreads();
+  }
+
   // (6) b and the radius of eq. (4).
   if (lane < GB) {
     const float *hs = F.hs + lane * kHs;
@@ -652,7 +843,7 @@ __device__ void finalize_empty(const AttendLaunch &L, int u, int h0) {
       if (L.radius) L.radius[uh0 + lane] = 0.0f;
     }
   }
-  if (lane == 0 && !L.plain) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+  if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
 }
 
 // One wave per (unit, split, head block).  Lane (g, c): MFMA column c is head slot c (weights for
@@ -667,7 +858,11 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   const int g = lane >> 4, c = lane & 15;
   const int64_t cbase = L.cap_off[u];
   const int64_t cap = L.cap_off[u + 1] - cbase;
-  const int cnt = (int)min(min((int64_t)L.count[u], cap), (int64_t)L.nsplit * L.split_rows);
+  const int64_t held = min((int64_t)L.count[u], cap);
+  const int cnt = (int)min(held, (int64_t)L.nsplit * L.split_rows);
+  if (L.status && sp == 0 && h0 == 0 && lane == 0 && !L.plain)
+    L.status[u] = ((int64_t)L.count[u] > cap ? EBD_ST_CAP_OVERFLOW : 0u) |
+                  (held > (int64_t)cnt ? EBD_ST_BAD_LAYOUT : 0u);
   const int row0 = sp * L.split_rows;
   if (row0 >= cnt) {  // empty split: the finalize skips it; an empty unit gets empty outputs
     if (L.nsplit == 1) finalize_empty<GB>(L, u, h0);
@@ -768,7 +963,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
       F.hs[(c - GB) * kHs + kHsC0] = s0;
       F.hs[(c - GB) * kHs + kHsC2] = s1;
     }
-    if (lane == 0 && !L.plain) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+    if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
     __syncthreads();
     const CandSrc C{s_chunk, 0, GB * kChunkFloats, kChunkFloats};
     finalize_block<GB>(L, u, h0, cnt, cbase, 1, C, F);
@@ -830,7 +1025,8 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
     finalize_empty<GB>(L, u, h0);
     return;
   }
-  if (lane == 0 && !L.plain) L.diag[(int64_t)u * L.nhb + h0 / kHeadBlock] = 0u;
+  if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
+  __syncthreads();  // the zeroed words are in place before the finalize's own updates
   const int nsp = (cnt + L.split_rows - 1) / L.split_rows;
   const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h0) * L.rec;  // (s, h) at s G rec + h rec
   const int64_t sstride = (int64_t)L.G * L.rec;
@@ -915,7 +1111,7 @@ size_t attend_finalize_lds(const AttendLaunch &L) {
 
 size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t split_rows) {
   const size_t nhb = (size_t)((G + kHeadBlock - 1) / kHeadBlock);
-  const size_t diag = ((size_t)U * nhb * sizeof(uint32_t) + 255) / 256 * 256;
+  const size_t diag = ((size_t)U * nhb * 2 * sizeof(uint32_t) + 255) / 256 * 256;
   if (nsplit <= 1) return diag;  // fused: no split records
   return diag + (size_t)U * (size_t)nsplit * (size_t)G * (size_t)attend_record_floats(split_rows) *
                     sizeof(float);

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -48,7 +49,7 @@ struct TimingRec {
   int64_t launches = 0;
 };
 std::mutex g_tmu;
-bool g_timing = false;
+std::atomic<bool> g_timing{false};
 std::map<std::string, TimingRec> g_trec;
 
 hipEvent_t pooled_event(TimingRec &r) {
@@ -64,7 +65,7 @@ hipEvent_t pooled_event(TimingRec &r) {
 
 template <class F>
 hipError_t timed(const char *name, hipStream_t s, F &&launch) {
-  if (!g_timing) return launch();
+  if (!g_timing.load(std::memory_order_acquire)) return launch();
   std::lock_guard<std::mutex> lk(g_tmu);
   TimingRec &r = g_trec[name];
   hipEvent_t a = pooled_event(r), b = pooled_event(r);
@@ -269,7 +270,7 @@ ebd_status ebd_evict(const ebd_evict_params *p, const float *scores, const uint1
 ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
                               const uint16_t *Vc, const float *pic, const int32_t *count,
                               float *y, float *vhat, float *lse, float *brange, float *radius,
-                              void *workspace, size_t ws_bytes, void *stream) {
+                              uint32_t *status, void *workspace, size_t ws_bytes, void *stream) {
   if (!valid_attend_params(p)) return EBD_ERR_INVALID_ARG;
   if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
   if (p->num_units == 0) return EBD_OK;
@@ -310,6 +311,7 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
   L.lse = lse;
   L.brange = brange;
   L.radius = radius;
+  L.status = status;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   L.plain = 0;
@@ -369,7 +371,8 @@ ebd_status ebd_block_contributions(const ebd_blocks_params *p, const uint16_t *q
       p->nblocks > kMaxBlocks || p->max_rows < 0 || p->scale < 0.0f || !std::isfinite(p->scale))
     return EBD_ERR_INVALID_ARG;
   if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
-  if (p->max_rows > ((int64_t)1 << 24)) return EBD_ERR_UNSUPPORTED;  // one wave reads a unit
+  // one wave reads a unit through 32-bit buffer ranges of 256-byte rows: 2^24 rows would wrap
+  if (p->max_rows >= ((int64_t)1 << 24)) return EBD_ERR_UNSUPPORTED;
   if (p->num_units == 0) return EBD_OK;
   if (!p->cap_off || !q || !Kc || !Vc || !pic || !idxc || !count || !y || !lse || !blocks)
     return EBD_ERR_INVALID_ARG;
@@ -457,7 +460,7 @@ ebd_status ebd_append_certain(int32_t num_units, int32_t head_dim, const int64_t
 
 ebd_status ebd_timing_enable(int32_t enable) {
   std::lock_guard<std::mutex> lk(g_tmu);
-  g_timing = enable != 0;
+  g_timing.store(enable != 0, std::memory_order_release);
   return EBD_OK;
 }
 

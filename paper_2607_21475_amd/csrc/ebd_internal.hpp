@@ -86,8 +86,9 @@ struct AttendLaunch {
   const float *pic;
   float scale, delta, eps0;
   float *part;          // [U * nsplit * G * rec]
-  uint32_t *diag;       // [0]: number of split rescans taken for the range term
+  uint32_t *diag;       // [U * nhb * 2]: range-term chunk rescans, heads with Vhat summed directly
   float *y, *vhat, *lse, *brange, *radius;
+  uint32_t *status;     // [U] or NULL: rows the step could not see (EBD_ST_*)
 };
 
 struct AppendLaunch {

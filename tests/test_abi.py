@@ -111,7 +111,7 @@ def test_attend_argument_validation():
         return p
 
     def call(p, ws=FAKE, ws_bytes=1 << 30):
-        return lib.ebd_attend_certify(ctypes.byref(p), *([FAKE] * 10), ws, ws_bytes, None)
+        return lib.ebd_attend_certify(ctypes.byref(p), *([FAKE] * 11), ws, ws_bytes, None)
 
     assert call(params(d=96)) == ebd.EBD_ERR_UNSUPPORTED
     assert call(params(G=0)) == ebd.EBD_ERR_INVALID_ARG
@@ -138,8 +138,8 @@ def test_workspace_sizes():
     def rec(split_rows):  # floats per record: sums, o, Cv, one block per 512-row chunk
         return 264 + 56 * ((split_rows + 511) // 512)
 
-    def counts(U, G):  # rescan counts per (unit, block of 8 query heads), 256-byte padded
-        return (4 * U * ((G + 7) // 8) + 255) // 256 * 256
+    def counts(U, G):  # two counts per (unit, block of 8 query heads), 256-byte padded
+        return (8 * U * ((G + 7) // 8) + 255) // 256 * 256
 
     # 1792 units fill the chip: one split each, finalized in the split kernel (no records)
     assert m == counts(1792, 7)
@@ -225,7 +225,11 @@ def test_finegrain_argument_validation():
     assert call(bp(d=64)) == ebd.EBD_ERR_UNSUPPORTED
     for bad in (dict(G=0), dict(rows=0), dict(nb=0), dict(nb=8193), dict(U=-1)):
         assert call(bp(**bad)) == ebd.EBD_ERR_INVALID_ARG, bad
+    # a unit's rows are addressed as 256-byte rows through 32-bit buffer ranges: 2^24 rows would
+    # wrap the range to 0, so the largest accepted unit is 2^24 - 1 rows
     assert call(bp(max_rows=(1 << 24) + 1)) == ebd.EBD_ERR_UNSUPPORTED
+    assert call(bp(max_rows=1 << 24)) == ebd.EBD_ERR_UNSUPPORTED
+    assert call(bp(max_rows=(1 << 24) - 1, nb=0)) == ebd.EBD_ERR_INVALID_ARG  # size itself accepted
     assert call(bp(U=0)) == ebd.EBD_OK
     c = ebd.ebd_cert_params()
     c.num_units, c.group, c.num_seqs, c.head_stride, c.unit_seq = 4, 7, 2, 0, FAKE

@@ -3,7 +3,9 @@
 Bars (stated in the design notes): pi within 1e-5 absolute; masks, compaction, counts and
 status bit-exact given the same fp32 pi (the GPU's pi is fed to the oracle's mask and
 compaction); yhat within 2e-3 relative (vector norm per query head); Vhat, b, r within 1e-2
-relative; ln Nhat within 1e-4 absolute.
+relative to max(|ref|, floor) with floors 1e-12 |yhat|^2, 1e-12 |yhat| and 1e-12 (so that a
+certificate that is zero up to fp32 underflow of tiny weights is not failed on round-off);
+ln Nhat within 1e-4 absolute.
 """
 import sys
 
@@ -35,6 +37,11 @@ def _np(t):
 
 def _bits(t):
     return synth.bf16_bits(t)
+
+
+def _cert_floor(key, ynorm):
+    """Absolute floor of the certificate tolerance: 1e-12 in the units of the quantity."""
+    return 1e-12 * (ynorm ** 2 if key == "vhat" else ynorm if key == "b" else np.ones_like(ynorm)) + 1e-300
 
 
 def _inputs(lengths, seed=0, group=1, scores="window", bad=None):
@@ -296,8 +303,7 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     assert np.all(y[empty] == 0)
     for key in ("vhat", "b", "r"):
         g, r = _np(res[key]).astype(np.float64), ref[key]
-        floor = 1e-6 * (nrm ** 2 if key == "vhat" else nrm) + 1e-30
-        bad = np.abs(g - r) > tol_c * np.maximum(np.abs(r), floor)
+        bad = np.abs(g - r) > tol_c * np.maximum(np.abs(r), _cert_floor(key, nrm))
         assert not bad.any(), (key, np.argwhere(bad)[:5], g[bad][:5], r[bad][:5])
     lse, lr = _np(res["lse"]).astype(np.float64), ref["lse"]
     assert np.all(np.isneginf(lse[empty]))
@@ -355,8 +361,7 @@ def test_attend_without_offset(lengths, G, split):
     for key in ("vhat", "b", "r"):  # the certificate does not depend on the flag
         np.testing.assert_array_equal(_np(res[key]), _np(ref_h[key]))
         g = _np(res[key]).astype(np.float64)
-        floor = 1e-6 * nrm ** (2 if key == "vhat" else 1) + 1e-30
-        assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.maximum(np.abs(ref[key]), floor)), key
+        assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.maximum(np.abs(ref[key]), _cert_floor(key, nrm))), key
 
 
 def test_attend_empty_and_tiny_units():
@@ -432,6 +437,151 @@ def test_attend_pi_one_is_full_attention():
     err = np.linalg.norm(_np(res["y"]) - yfull, axis=2) / np.linalg.norm(yfull, axis=2)
     assert np.max(err) <= 2e-3
     assert np.all(_np(res["vhat"]) == 0) and np.all(_np(res["b"]) == 0) and np.all(_np(res["r"]) == 0)
+
+
+@pytest.mark.parametrize("scores,G,split", [("window", 4, 0), ("pareto", 4, 0), ("window", 7, 256)])
+def test_attend_paper_floor_1e6(scores, G, split):
+    """The paper's floor pi_min = 1e-6 (Sec. 3.3 eq. (2)), so 1/pi reaches 1e6.  Neither score
+    recipe gets near it by itself (window scores vary by a few-fold, Pareto scores are >= 1), so
+    a random 30% of the tokens have their score scaled down log-uniformly by up to 1e7 (tokens
+    the window barely attends to): their pi then spans 1e-6 .. 0.1, and some are retained."""
+    _say("attend floor 1e-6 scores=%s G=%d split=%d" % (scores, G, split))
+    from paper_2607_21475_amd import cache
+
+    lengths = [6144] * 48
+    K, V, seq_off, sc, q = _inputs(lengths, seed=41, group=G, scores=scores)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(43)
+    low = torch.rand(sc.shape, generator=g, device="cuda") < 0.3
+    f = torch.pow(10.0, -7.0 * torch.rand(sc.shape, generator=g, device="cuda"))
+    sc = torch.where(low, sc * f, sc)
+    out = _evict(K, V, seq_off, sc, lengths, budget_frac=0.1, pi_min=1e-6, seed=17)
+    _check_evict(lengths, K, V, seq_off, sc, out, budget=0.1, pi_min=1e-6, seed=17)
+    assert (_np(out.pi_full)[: 6144 * 48] == np.float32(1e-6)).sum() > 1000  # the floor binds
+    res = cache.attend_certify(out, q, split_rows=split)
+    torch.cuda.synchronize()
+    _check_attend(out, res, q, G)
+    assert not _np(res["status"]).any()
+    coff, cnt = _np(out.cap_off), _np(out.count)
+    pic = _np(out.pic)
+    kept = np.concatenate([pic[coff[u]:coff[u] + cnt[u]] for u in range(len(lengths))])
+    assert kept.min() < 1e-3  # rows drawn close to the floor are retained
+
+
+def _retained_cache(units, extra_cap=0):
+    """A compacted cache laid out as ebd_evict writes it, from per-unit host arrays (Kc, Vc bf16
+    bits [c, 128], pi fp32 [c]): capacity = c + extra_cap rows, count = c."""
+    from paper_2607_21475_amd import cache
+
+    caps = [len(p) + extra_cap for _, _, p in units]
+    off = np.concatenate([[0], np.cumsum(caps)]).astype(np.int64)
+    rows = int(off[-1])
+    Kc = np.zeros((rows, 128), np.uint16)
+    Vc = np.zeros((rows, 128), np.uint16)
+    pic = np.ones(rows, np.float32)
+    for u, (k, v, p) in enumerate(units):
+        a = off[u]
+        Kc[a:a + len(p)], Vc[a:a + len(p)], pic[a:a + len(p)] = k, v, p
+    dev = "cuda"
+    as_bf16 = lambda x: torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)  # noqa: E731
+    return cache.RetainedCache(
+        Kc=as_bf16(Kc), Vc=as_bf16(Vc), pic=torch.from_numpy(pic).to(dev),
+        idxc=torch.zeros(rows, dtype=torch.int32, device=dev),
+        count=torch.tensor([len(p) for _, _, p in units], dtype=torch.int32, device=dev),
+        status=torch.zeros(len(units), dtype=torch.int32, device=dev),
+        cap_off=torch.from_numpy(off).to(dev), max_cap=max(caps))
+
+
+def _dominated_unit(rng, n, G, q, boost, pi_floor=1e-6, tail_pi=(0.05, 1.0)):
+    """n retained rows: 68 certain, the rest a tail with pi in tail_pi, and one row j drawn at the
+    floor whose key is pushed along q's first head so that its Hajek weight a_j / pi_j exceeds the
+    rest of Nhat by a large factor (the cancellation case of the one-pass variance)."""
+    from helpers import bf16_to_f64, rand_bf16, to_bf16_bits
+
+    K = rand_bf16(rng, (n, 128))
+    V = rand_bf16(rng, (n, 128))
+    pi = rng.uniform(*tail_pi, n).astype(np.float32)
+    pi[:68] = 1.0
+    j = n // 2
+    qf = bf16_to_f64(q[0])
+    K[j] = to_bf16_bits(bf16_to_f64(K[j]) + boost * qf / np.linalg.norm(qf))
+    pi[j] = pi_floor
+    return K, V, pi
+
+
+@pytest.mark.parametrize("G,n,boost,split", [
+    (1, 600, 0.0, 0),     # 1/pi = 1e6 alone: the floor row outweighs the rest of Nhat ~3e2-fold
+    (4, 1500, 4.0, 0),    # its key also aligned with head 0's query: ~7e3-fold for that head
+    (7, 3000, 3.0, 0),
+    (4, 5000, 4.5, 512),  # several splits: the direct sum runs in attend_finalize
+    (8, 900, 2.0, 128),
+    (4, 1500, 9.0, 0),    # 1e5 to 1e7-fold: the floor row alone makes yhat to fp32 precision
+])
+def test_attend_vhat_cancellation_direct_sum(G, n, boost, split):
+    """A floor row (pi = 1e-6) retained and dominating Nhat: yhat ~ v_j, so C2 - 2 yhat.Cv +
+    |yhat|^2 C0 cancels by many orders of magnitude.  The finalize detects it and sums Vhat
+    directly; Vhat, b and r must match the oracle's two-pass definition."""
+    _say("attend vhat cancellation G=%d n=%d boost=%s split=%d" % (G, n, boost, split))
+    from paper_2607_21475_amd import cache
+    from helpers import rand_bf16
+
+    rng = np.random.default_rng(100 + G)
+    U = 6
+    q = rand_bf16(rng, (U, G, 128))
+    units = [_dominated_unit(rng, n, G, q[u], boost) for u in range(U - 1)]
+    units.append((rand_bf16(rng, (n, 128)), rand_bf16(rng, (n, 128)),
+                  rng.uniform(0.05, 1.0, n).astype(np.float32)))  # an ordinary unit beside them
+    rc = _retained_cache(units)
+    qt = torch.from_numpy(q.view(np.int16)).cuda().view(torch.bfloat16)
+    res = cache.attend_certify(rc, qt, split_rows=split)
+    torch.cuda.synchronize()
+    ref = _check_attend(rc, res, qt, G)
+    assert cache.direct_variances(res["ws"], U, G) >= U - 1
+    # the dominated units really are in the cancelling regime: head 0's Vhat is far below the
+    # scale |v_j|^2 of the dominating row's own C2 term (more than 6 bits cancel)
+    from helpers import bf16_to_f64
+
+    vj2 = np.array([np.sum(bf16_to_f64(Vu[n // 2]) ** 2) for _, Vu, _ in units[:U - 1]])
+    assert np.all(ref["vhat"][: U - 1, 0] < vj2 / 64)
+
+
+def test_attend_status_reports_unseen_rows():
+    """Rows the step cannot see are reported, never silently dropped: a count above the unit's
+    capacity (EBD_ST_CAP_OVERFLOW) and units longer than the planned max_rows (EBD_ST_BAD_LAYOUT).
+    The outputs cover the rows seen, as the oracle computes them over those rows."""
+    _say("attend status")
+    import dataclasses
+
+    from paper_2607_21475_amd import cache
+    from helpers import rand_bf16
+
+    rng = np.random.default_rng(7)
+    G, sizes = 2, [300, 40, 700, 96]
+    units = [(rand_bf16(rng, (c, 128)), rand_bf16(rng, (c, 128)),
+              rng.uniform(0.05, 1.0, c).astype(np.float32)) for c in sizes]
+    rc = _retained_cache(units)
+    q = rand_bf16(rng, (len(sizes), G, 128))
+    qt = torch.from_numpy(q.view(np.int16)).cuda().view(torch.bfloat16)
+    res = cache.attend_certify(rc, qt)
+    torch.cuda.synchronize()
+    assert not _np(res["status"]).any()
+    # unit 1 claims 5 rows beyond its capacity
+    rc.count[1] += 5
+    res = cache.attend_certify(rc, qt)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_np(res["status"]), [0, 1, 0, 0])
+    rc.count[1] -= 5
+    # a plan for at most 128 rows: units 0 and 2 are longer
+    short = dataclasses.replace(rc, max_cap=128)
+    res = cache.attend_certify(short, qt)
+    torch.cuda.synchronize()
+    st = _np(res["status"])
+    np.testing.assert_array_equal(st & 16, [16, 0, 16, 0])
+    seen = [min(c, 128) for c in sizes]  # the planner's single 128-row split per unit
+    for u, (k, v, p) in enumerate(units):
+        ref = oracle.attend_certify(q[u], k[:seen[u]], v[:seen[u]], p[:seen[u]])
+        y = _np(res["y"][u]).astype(np.float64)
+        assert np.all(np.linalg.norm(y - ref["y"], axis=1) <= 2e-3 * np.linalg.norm(ref["y"], axis=1))
 
 
 def test_append_certain():
@@ -571,7 +721,7 @@ def _check_unit_attend(u, q, res, Kc_r, Vc_r, pic_r):
     assert np.all(err <= 2e-3), (u, err)
     for key in ("vhat", "b", "r"):
         g = _np(res[key][u]).astype(np.float64)
-        floor = 1e-6 * np.linalg.norm(ref["y"], axis=1) ** (2 if key == "vhat" else 1)
+        floor = _cert_floor(key, np.linalg.norm(ref["y"], axis=1))
         assert np.all(np.abs(g - ref[key]) <= 1e-2 * np.maximum(np.abs(ref[key]), floor)), (key, u, g, ref[key])
     lse = _np(res["lse"][u]).astype(np.float64)
     assert np.all(np.abs(lse - ref["lse"]) <= 1e-4 * np.maximum(1.0, np.abs(ref["lse"])))
