@@ -9,7 +9,7 @@ error statuses.  The functions carry the C names:
     ebd_append_certain   append a decode token with pi = 1
     ebd_workspace_size, ebd_status_string, ebd_version, ebd_timing_enable, ebd_timing_read
 
-The library must be built (``python -m paper_2607_21475_amd.build``); importing this package
+The library must be built (``python paper_2607_21475_amd/build.py``); importing this package
 without it raises, and there is no other implementation to fall back to.
 """
 from __future__ import annotations
@@ -23,7 +23,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libebd.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libebd.so is not built (run python -m paper_2607_21475_amd.build); "
+    raise ImportError("libebd.so is not built (run python paper_2607_21475_amd/build.py); "
                       "the EBD path has no fallback")
 _lib = ctypes.CDLL(LIB_PATH)
 

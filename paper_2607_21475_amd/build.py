@@ -1,6 +1,8 @@
 """Build libebd.so (gfx950) in-tree with hipcc.
 
-    python -m paper_2607_21475_amd.build
+    python paper_2607_21475_amd/build.py
+
+(run as a file: importing the package loads the previously built library.)
 
 Objects go to _build/ at the repository root; the shared library is written next to this file.
 """
