@@ -200,6 +200,31 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
                               uint32_t *status, void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * ebd_attend_certify_noalloc -- ebd_attend_certify for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * same arguments, outputs and kernels, without the workspace argument.  The workspace is a fixed
+ * device array inside the library of EBD_NOALLOC_SCRATCH_BYTES (64 MiB), one copy per GPU that
+ * loads the library, held until the process ends.  The call allocates nothing and frees nothing
+ * (host or device), and is not recorded by the kernel timing below.
+ *   Returns EBD_ERR_UNSUPPORTED when the launch needs more than EBD_NOALLOC_SCRATCH_BYTES, i.e.
+ *   when ebd_workspace_size(EBD_WS_ATTEND, p) exceeds it (nothing is launched); use
+ *   ebd_attend_certify with a caller workspace for such launches.  Launches whose units are
+ *   each one split need only 8 bytes per (unit, block of 8 query heads).
+ *   Every call on one GPU uses that GPU's one array: calls that overlap on the same GPU (on
+ *   several streams or from several host threads) race and must be ordered by the caller, e.g.
+ *   issued on one stream.  The array keeps the last call's contents; nothing in it has to be
+ *   cleared between calls.  The diagnostic counts that ebd_attend_certify leaves at the start
+ *   of its workspace stay inside the library here.
+ */
+#define EBD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+ebd_status ebd_attend_certify_noalloc(const ebd_attend_params *p, const uint16_t *q,
+                                      const uint16_t *Kc, const uint16_t *Vc, const float *pic,
+                                      const int32_t *count, float *y, float *vhat, float *lse,
+                                      float *brange, float *radius, uint32_t *status,
+                                      void *stream);
+
+/*
  * ebd_append_certain -- append one decode token per unit to its retained set with pi = 1
  * (a recency-certainty token; the sampled draw is reused across steps, App. A.2).
  *   k_new, v_new [U, 128] bf16; pos_new [U] int32 original positions or NULL (idx = -1).

@@ -50,6 +50,7 @@ EBD_WS_EVICT = 0
 EBD_WS_ATTEND = 1
 EBD_WS_SCORES = 2
 EBD_SCORES_ACCUMULATE = 1
+EBD_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 HEAD_DIM = 128
 
@@ -134,6 +135,8 @@ _lib.ebd_evict.restype = ctypes.c_int
 _lib.ebd_attend_certify.argtypes = [ctypes.POINTER(ebd_attend_params)] + [_P] * 12 + \
     [ctypes.c_size_t, _P]
 _lib.ebd_attend_certify.restype = ctypes.c_int
+_lib.ebd_attend_certify_noalloc.argtypes = [ctypes.POINTER(ebd_attend_params)] + [_P] * 12
+_lib.ebd_attend_certify_noalloc.restype = ctypes.c_int
 _lib.ebd_scores.argtypes = [ctypes.POINTER(ebd_scores_params)] + [_P] * 4 + [ctypes.c_size_t, _P]
 _lib.ebd_scores.restype = ctypes.c_int
 _lib.ebd_block_contributions.argtypes = [ctypes.POINTER(ebd_blocks_params)] + [_P] * 10
@@ -284,6 +287,21 @@ def ebd_attend_certify(params: ebd_attend_params, q, Kc, Vc, pic, count, y, vhat
                                    _ptr(workspace, None, "workspace"),
                                    workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ebd_attend_certify", code)
+
+
+def ebd_attend_certify_noalloc(params: ebd_attend_params, q, Kc, Vc, pic, count, y, vhat, lse,
+                               brange=None, radius=None, status=None, stream=None) -> None:
+    """The same step without a workspace argument (the library's fixed per-GPU scratch array)."""
+    bf = torch.bfloat16
+    f32 = torch.float32
+    code = _lib.ebd_attend_certify_noalloc(ctypes.byref(params), _ptr(q, bf, "q"),
+                                           _ptr(Kc, bf, "Kc"), _ptr(Vc, bf, "Vc"),
+                                           _ptr(pic, f32, "pic"), _ptr(count, torch.int32, "count"),
+                                           _ptr(y, f32, "y"), _ptr(vhat, f32, "vhat"),
+                                           _ptr(lse, f32, "lse"), _ptr(brange, f32, "brange"),
+                                           _ptr(radius, f32, "radius"),
+                                           _ptr(status, torch.int32, "status"), _stream(stream))
+    _check("ebd_attend_certify_noalloc", code)
 
 
 def ebd_scores(params: ebd_scores_params, q, K, scores, workspace, stream=None) -> None:

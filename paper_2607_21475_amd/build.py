@@ -20,7 +20,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libebd.so")
 
-SOURCES = ["evict.hip", "attend.hip", "append.hip", "scores.hip", "finegrain.hip", "ebd_api.cpp"]
+SOURCES = ["evict.hip", "attend.hip", "append.hip", "scores.hip", "finegrain.hip", "noalloc.hip",
+           "ebd_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed fp32 ops are disabled in every kernel (some of their forms have been unreliable).

@@ -178,6 +178,80 @@ bool valid_attend_params(const ebd_attend_params *p) {
 
 }  // namespace
 
+namespace ebd {
+
+ebd_status device_ok() { return check_device(); }
+
+ebd_status attend_check(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
+                        const uint16_t *Vc, const float *pic, const int32_t *count, const float *y,
+                        const float *vhat, const float *lse, size_t *need) {
+  if (!valid_attend_params(p)) return EBD_ERR_INVALID_ARG;
+  if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
+  *need = 0;
+  if (p->num_units == 0) return EBD_OK;
+  if (!q || !Kc || !Vc || !pic || !count || !y || !vhat || !lse) return EBD_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(pic, 4) ||
+      !aligned(y, 16))
+    return EBD_ERR_INVALID_ARG;
+  const int32_t sr = attend_split_rows(p);
+  if (attend_nsplit(p, sr) > kMaxSplits) return EBD_ERR_UNSUPPORTED;
+  *need = attend_workspace_bytes(p->num_units, attend_nsplit(p, sr), p->group, sr);
+  return EBD_OK;
+}
+
+ebd_status attend_launch(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
+                         const uint16_t *Vc, const float *pic, const int32_t *count, float *y,
+                         float *vhat, float *lse, float *brange, float *radius, uint32_t *status,
+                         void *workspace, void *stream, bool timing) {
+  const int32_t sr = attend_split_rows(p);
+  const int32_t nsplit = attend_nsplit(p, sr);
+  AttendLaunch L;
+  L.U = p->num_units;
+  L.G = p->group;
+  L.nsplit = nsplit;
+  L.split_rows = sr;
+  L.nchunk = attend_chunks(sr);
+  L.rec = attend_record_floats(sr);
+  L.nhb = (p->group + kHeadBlock - 1) / kHeadBlock;
+  L.cap_off = p->cap_off;
+  L.count = count;
+  L.q = q;
+  L.Kc = Kc;
+  L.Vc = Vc;
+  L.pic = pic;
+  L.scale = p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)kHeadDim);
+  L.delta = p->delta > 0.0f ? p->delta : 0.1f;
+  L.eps0 = p->eps0 > 0.0f ? p->eps0 : 1e-9f;
+  char *ws = static_cast<char *>(workspace);
+  L.diag = reinterpret_cast<uint32_t *>(ws);
+  L.part = reinterpret_cast<float *>(ws + attend_workspace_bytes(p->num_units, 1, p->group, sr));
+  L.y = y;
+  L.vhat = vhat;
+  L.lse = lse;
+  L.brange = brange;
+  L.radius = radius;
+  L.status = status;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  L.plain = 0;
+  const int passes = (p->flags & EBD_F_NO_OFFSET) ? 2 : 1;
+  for (int pass = 0; pass < passes; ++pass) {
+    L.plain = pass;  // the second pass replaces y and ln N by the uncorrected softmax
+    const hipError_t e1 = timing ? timed("attend_split", s, [&] { return launch_attend_split(L, s); })
+                                 : launch_attend_split(L, s);
+    if (e1 != hipSuccess) return EBD_ERR_HIP;
+    if (L.nsplit > 1) {
+      const hipError_t e2 =
+          timing ? timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); })
+                 : launch_attend_finalize(L, s);
+      if (e2 != hipSuccess) return EBD_ERR_HIP;
+    }
+  }
+  return EBD_OK;
+}
+
+}  // namespace ebd
+
 extern "C" {
 
 const char *ebd_version(void) { return "ebd-gfx950 0.1.0"; }
@@ -271,60 +345,14 @@ ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, con
                               const uint16_t *Vc, const float *pic, const int32_t *count,
                               float *y, float *vhat, float *lse, float *brange, float *radius,
                               uint32_t *status, void *workspace, size_t ws_bytes, void *stream) {
-  if (!valid_attend_params(p)) return EBD_ERR_INVALID_ARG;
-  if (p->head_dim != kHeadDim) return EBD_ERR_UNSUPPORTED;
-  if (p->num_units == 0) return EBD_OK;
-  if (!q || !Kc || !Vc || !pic || !count || !y || !vhat || !lse) return EBD_ERR_INVALID_ARG;
-  if (!aligned(q, 16) || !aligned(Kc, 16) || !aligned(Vc, 16) || !aligned(pic, 4) ||
-      !aligned(y, 16))
-    return EBD_ERR_INVALID_ARG;
-  const int32_t sr = attend_split_rows(p);
-  const int32_t nsplit = attend_nsplit(p, sr);
-  if (nsplit > kMaxSplits) return EBD_ERR_UNSUPPORTED;
-  const size_t need = attend_workspace_bytes(p->num_units, nsplit, p->group, sr);
+  size_t need = 0;
+  const ebd_status cs = ebd::attend_check(p, q, Kc, Vc, pic, count, y, vhat, lse, &need);
+  if (cs != EBD_OK || p->num_units == 0) return cs;
   if (!workspace || ws_bytes < need || !aligned(workspace, 256)) return EBD_ERR_WORKSPACE;
   const ebd_status ds = check_device();
   if (ds != EBD_OK) return ds;
-
-  AttendLaunch L;
-  L.U = p->num_units;
-  L.G = p->group;
-  L.nsplit = nsplit;
-  L.split_rows = sr;
-  L.nchunk = attend_chunks(sr);
-  L.rec = attend_record_floats(sr);
-  L.nhb = (p->group + kHeadBlock - 1) / kHeadBlock;
-  L.cap_off = p->cap_off;
-  L.count = count;
-  L.q = q;
-  L.Kc = Kc;
-  L.Vc = Vc;
-  L.pic = pic;
-  L.scale = p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)kHeadDim);
-  L.delta = p->delta > 0.0f ? p->delta : 0.1f;
-  L.eps0 = p->eps0 > 0.0f ? p->eps0 : 1e-9f;
-  char *ws = static_cast<char *>(workspace);
-  L.diag = reinterpret_cast<uint32_t *>(ws);
-  L.part = reinterpret_cast<float *>(ws + attend_workspace_bytes(p->num_units, 1, p->group, sr));
-  L.y = y;
-  L.vhat = vhat;
-  L.lse = lse;
-  L.brange = brange;
-  L.radius = radius;
-  L.status = status;
-
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  L.plain = 0;
-  const int passes = (p->flags & EBD_F_NO_OFFSET) ? 2 : 1;
-  for (int pass = 0; pass < passes; ++pass) {
-    L.plain = pass;  // the second pass replaces y and ln N by the uncorrected softmax
-    if (timed("attend_split", s, [&] { return launch_attend_split(L, s); }) != hipSuccess)
-      return EBD_ERR_HIP;
-    if (L.nsplit > 1 &&
-        timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); }) != hipSuccess)
-      return EBD_ERR_HIP;
-  }
-  return EBD_OK;
+  return ebd::attend_launch(p, q, Kc, Vc, pic, count, y, vhat, lse, brange, radius, status,
+                            workspace, stream, true);
 }
 
 ebd_status ebd_scores(const ebd_scores_params *p, const uint16_t *q, const uint16_t *K,

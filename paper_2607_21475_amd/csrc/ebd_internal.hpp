@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "ebd.h"
+
 namespace ebd {
 
 constexpr int kHeadDim = 128;                // rows of K, V and q are 128 bf16
@@ -140,6 +142,17 @@ size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t spli
 size_t attend_fused_lds_bytes(int32_t split_rows, int gb);  // LDS of a split that also finalizes
 size_t attend_part_lds_bytes(int32_t split_rows, int gb);   // LDS of one split of several
 size_t scores_workspace_bytes(int32_t U, int32_t nsplit, int32_t W);
+
+// The attention entry points' shared parts (ebd_api.cpp): argument checks (need = workspace
+// bytes the launch uses), the device check, and the launches on a given workspace.
+ebd_status attend_check(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
+                        const uint16_t *Vc, const float *pic, const int32_t *count, const float *y,
+                        const float *vhat, const float *lse, size_t *need);
+ebd_status device_ok();
+ebd_status attend_launch(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
+                         const uint16_t *Vc, const float *pic, const int32_t *count, float *y,
+                         float *vhat, float *lse, float *brange, float *radius, uint32_t *status,
+                         void *workspace, void *stream, bool timing);
 
 hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s);
 hipError_t launch_evict_copy(const EvictLaunch &L, hipStream_t s);

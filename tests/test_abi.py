@@ -278,3 +278,25 @@ def test_capacity_plan_covers_floor_and_protected():
     assert cache.unit_capacity(0, 0.5, 0, extra=3) == 16
     off = cache.plan_capacity([300, 0, 6144], [0.1, 0.5, 0.25], 4, 64)
     assert off[0] == 0 and off[1] >= 80 and off[2] == off[1] and off[3] > off[2]
+
+
+def test_noalloc_argument_validation():
+    """The entry point without allocation validates like ebd_attend_certify and rejects launches
+    whose workspace would exceed its fixed scratch array, before touching the device."""
+    ebd, lib = _lib()
+    p = ebd.ebd_attend_params()
+    p.num_units, p.group, p.head_dim, p.max_rows, p.cap_off, p.delta = 4, 4, 128, 2000, FAKE, 0.1
+
+    def call(p):
+        return lib.ebd_attend_certify_noalloc(ctypes.byref(p), *([FAKE] * 11), None)
+
+    assert lib.ebd_attend_certify_noalloc(None, *([FAKE] * 11), None) == ebd.EBD_ERR_INVALID_ARG
+    p.head_dim = 64
+    assert call(p) == ebd.EBD_ERR_UNSUPPORTED
+    p.head_dim, p.group = 128, 0
+    assert call(p) == ebd.EBD_ERR_INVALID_ARG
+    p.group, p.num_units = 4, 0
+    assert call(p) == ebd.EBD_OK
+    p.num_units, p.group, p.max_rows, p.split_rows = 200000, 8, 4096, 16
+    assert ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, p) > ebd.EBD_NOALLOC_SCRATCH_BYTES
+    assert call(p) == ebd.EBD_ERR_UNSUPPORTED
