@@ -78,6 +78,7 @@ __device__ __forceinline__ void load_tile(Tile &T, __amdgpu_buffer_rsrc_t rK, __
 struct SplitState {
   f32x4 acc[8];
   float mrun, s0, s1;
+  float pl;  // logit of this lane's head's current pivot (-inf: none yet)
   float ck[4], cg[4], dk, dg;  // candidate lists (descending g^2 |v|^2, with g^2) and dropped maxima
   int cr[4];
 };
@@ -87,11 +88,26 @@ struct SplitState {
 // cross-lane max.
 constexpr float kLazy = 8.0f;
 
+// Pivot rows.  One row that outweighs the rest of a head makes yhat ~ its v, and then the one-pass
+// C2 - 2 yhat.Cv + |yhat|^2 C0 cancels (a row drawn near a small floor carries 1/pi up to 1e6).
+// So each head keeps its largest-weight row out of every sum: a row becomes the head's pivot when
+// its logit exceeds the current pivot's by more than kPivGap (a factor 8 in weight), is recorded
+// in the head's list (row, logit, pi) and gets weight 0 in the sums and the candidate lists.  A
+// row that outweighs every other row by more than 8x is then the last pivot, whatever the order;
+// the finalize adds the earlier pivots back exactly and treats the last one in closed form.  With
+// the gap, a head takes a new pivot a few times per split at most (the first tile always).
+constexpr float kPivGap = 3.0f;
+
 // One 16-row tile: rows 16t + 4g + i of the split for this lane's head slot; `nvalid` rows of the
 // lane's row group are real (<= 0 masks them all), `rowbase` is the unit row of its first one.
+// kPivLogit: the slot of a pivot list that holds the head's current pivot logit when it is kept in
+// LDS rather than in a register (the eight-head kernel, whose registers are otherwise exhausted).
+constexpr int kPivLogit = 25;
+
+template <bool PL_LDS>
 __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const bf16x8 (&qop)[4],
                                            int nvalid, int rowbase, bool isC, bool plain,
-                                           float scale2) {
+                                           float scale2, float *s_piv, int hslot, bool isW) {
   f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
@@ -110,7 +126,37 @@ __device__ __forceinline__ void split_tile(SplitState &S, const Tile &T, const b
   float lg[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) lg[i] = i < nvalid ? fmaf(sacc[i], scale2, -lp[i]) : -INFINITY;
-  const float lmax = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
+  float lmax = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
+  const float pl = PL_LDS ? s_piv[hslot * kPivFloats + kPivLogit] : S.pl;
+  if (__any(lmax > pl + kPivGap)) {
+    // a new pivot for some head: the tile's largest logit of each column and its row (the lowest
+    // of equal ones); both columns of a head see the same logits and decide alike
+    const int g = __lane_id() >> 4;
+    float tm = fmaxf(lmax, __shfl_xor(lmax, 16));
+    tm = fmaxf(tm, __shfl_xor(tm, 32));
+    int r = 16;
+#pragma unroll
+    for (int i = 3; i >= 0; --i) r = (lg[i] == tm) ? 4 * g + i : r;
+    r = min(r, __shfl_xor(r, 16));
+    r = min(r, __shfl_xor(r, 32));
+    const int rr = r & 15;
+    const int pn = __float_as_int(s_piv[hslot * kPivFloats]);  // the list's count
+    if (tm > pl + kPivGap && pn < kPivMax) {
+      if (isW && g == (rr >> 2)) {  // the weight lane holding the row records it
+        float *e = s_piv + hslot * kPivFloats;
+        const float pa = (rr & 1) ? T.p[1] : T.p[0], pb = (rr & 1) ? T.p[3] : T.p[2];
+        e[1 + 3 * pn] = __int_as_float(rowbase - 4 * g + rr);
+        e[2 + 3 * pn] = tm;
+        e[3 + 3 * pn] = (rr & 2) ? pb : pa;
+        e[0] = __int_as_float(pn + 1);
+        if (PL_LDS) e[kPivLogit] = tm;
+      }
+      if (!PL_LDS) S.pl = tm;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lg[i] = (g == (rr >> 2) && i == (rr & 3)) ? -INFINITY : lg[i];
+      lmax = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
+    }
+  }
   if (__any(lmax > S.mrun + kLazy)) {
     float tmax = fmaxf(lmax, __shfl_xor(lmax, 16));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
@@ -284,12 +330,15 @@ __device__ __forceinline__ void flush_chunk(SplitState &S, float *s_chunk, int k
 // the radius r, from the combined sums in LDS and the candidate blocks of every chunk.
 // ---------------------------------------------------------------------------------------------
 constexpr int kListCap = 256;  // candidates evaluated per batch
-constexpr int kHs = 8;         // per-head table: M, l, C0, C2, |yhat|, lb, Vhat, redo
+// per-head table: M, l, C0, C2, |yhat|, lb, Vhat, redo, then the pivot: logit (-inf: none), pi,
+// row, key (split * kPivMax + entry)
+constexpr int kHs = 12;
 constexpr int kHsM = 0, kHsL = 1, kHsC0 = 2, kHsC2 = 3, kHsYn = 4, kHsLb = 5, kHsV = 6, kHsRedo = 7;
+constexpr int kHsPl = 8, kHsPp = 9, kHsPr = 10, kHsPk = 11;
 // The one-pass form C2 - 2 yhat.Cv + |yhat|^2 C0 of sum c |v - yhat|^2 carries a rounding error of
 // a few ulps of (sqrt(C2) + |yhat| sqrt(C0))^2 (each sum is of exact products, rounded in fp32);
 // below this fraction of that scale the head's Vhat is summed again directly.
-constexpr float kCancelFrac = 1.0f / 64.0f;
+constexpr float kCancelFrac = 1.0f / 1024.0f;
 
 // Per (unit, head block) diagnostic words at the start of the workspace: the 512-row chunks
 // rescanned for the range term, and the heads whose Vhat was summed directly.
@@ -324,51 +373,202 @@ struct CandSrc {
   int kstride, hstride;
 };
 
+// Where the pivot list of (split s, head h) lives: LDS for a fused split, the records otherwise.
+struct PivSrc {
+  const float *base;
+  int64_t sstride;
+  int hstride;
+  __device__ const float *at(int s, int h) const { return base + s * sstride + h * hstride; }
+};
+
+// Calls f(row, logit, pi, key) for every pivot entry of head h over the splits, in a fixed order
+// (split, entry); key = split * kPivMax + entry.  All lanes of a head run the same iterations.
+template <class Fn>
+__device__ __forceinline__ void for_each_pivot(const PivSrc &P, int nsp, int h, bool act, Fn &&f) {
+  for (int s = 0; s < nsp; ++s) {
+    const float *pl = P.at(s, h);
+    const int n = act ? __float_as_int(pl[0]) : 0;
+#pragma unroll
+    for (int e = 0; e < kPivMax; ++e)
+      if (e < n) f(__float_as_int(pl[1 + 3 * e]), pl[2 + 3 * e], pl[3 + 3 * e], s * kPivMax + e);
+  }
+}
+
+// Before the finalize: per head, the entry with the largest logit over all splits becomes the
+// pivot (kept in the head's table), the running max is raised to its logit if needed (the sums
+// rescaled), and every other entry is added back into l, o, C0, Cv, C2 exactly.  8 lanes per
+// head, 16 dims per lane.
+template <int GB>
+__device__ void pivot_prepare(const AttendLaunch &L, int64_t cbase, int nsp, const PivSrc &P,
+                              const FinLds<GB> &F) {
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 3, j = lane & 7;
+  const bool act = h < GB;
+  const int hh = act ? h : 0;
+  __syncthreads();  // the sums are in LDS
+  // the pivot: lanes of a head look at every eighth split, then compare
+  float bl = -INFINITY;
+  int bk = 0x7fffffff;
+  for (int s = j; s < nsp; s += 8) {
+    const float *pl = P.at(s, hh);
+    const int n = act ? __float_as_int(pl[0]) : 0;
+#pragma unroll
+    for (int e = 0; e < kPivMax; ++e) {
+      if (e < n && pl[2 + 3 * e] > bl) {
+        bl = pl[2 + 3 * e];
+        bk = s * kPivMax + e;
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) {
+    const float ol = __shfl_xor(bl, o);
+    const int ok = __shfl_xor(bk, o);
+    if (ol > bl || (ol == bl && ok < bk)) {
+      bl = ol;
+      bk = ok;
+    }
+  }
+  float *hs = F.hs + hh * kHs;
+  const float M0 = hs[kHsM], M1 = fmaxf(M0, bl);
+  const float f = scale_of(M0, M1), f2 = f * f;
+  float o16[16], c16[16];
+  {
+    const float4 *op = reinterpret_cast<const float4 *>(F.o + hh * kHeadDim + 16 * j);
+    const float4 *cp = reinterpret_cast<const float4 *>(F.o + (GB + hh) * kHeadDim + 16 * j);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 a = op[q], b = cp[q];
+      o16[4 * q] = a.x * f, o16[4 * q + 1] = a.y * f, o16[4 * q + 2] = a.z * f, o16[4 * q + 3] = a.w * f;
+      c16[4 * q] = b.x * f2, c16[4 * q + 1] = b.y * f2, c16[4 * q + 2] = b.z * f2, c16[4 * q + 3] = b.w * f2;
+    }
+  }
+  float la = 0.0f, c0a = 0.0f, c2a = 0.0f;
+  for_each_pivot(P, nsp, hh, act, [&](int row, float lgt, float p, int key) {
+    if (key == bk) return;
+    const float w = fast_exp2(lgt - M1), cc = (1.0f - p) * w * w;
+    const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + row) * kHeadDim + 16 * j);
+    const uint4 va = vr[0], vb = vr[1];
+    const uint32_t vw[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+    float nv = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const float x0 = bf16_lo(vw[t]), x1 = bf16_hi(vw[t]);
+      o16[2 * t] = fmaf(w, x0, o16[2 * t]);
+      o16[2 * t + 1] = fmaf(w, x1, o16[2 * t + 1]);
+      c16[2 * t] = fmaf(cc, x0, c16[2 * t]);
+      c16[2 * t + 1] = fmaf(cc, x1, c16[2 * t + 1]);
+      nv = fmaf(x0, x0, nv);
+      nv = fmaf(x1, x1, nv);
+    }
+    nv += __shfl_xor(nv, 1);
+    nv += __shfl_xor(nv, 2);
+    nv += __shfl_xor(nv, 4);
+    la += w;
+    c0a += cc;
+    c2a = fmaf(cc, nv, c2a);
+  });
+  __syncthreads();  // every lane has read the sums it rescales
+  if (act) {
+    float4 *op = reinterpret_cast<float4 *>(F.o + hh * kHeadDim + 16 * j);
+    float4 *cp = reinterpret_cast<float4 *>(F.o + (GB + hh) * kHeadDim + 16 * j);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      op[q] = make_float4(o16[4 * q], o16[4 * q + 1], o16[4 * q + 2], o16[4 * q + 3]);
+      cp[q] = make_float4(c16[4 * q], c16[4 * q + 1], c16[4 * q + 2], c16[4 * q + 3]);
+    }
+    if (j == 0) {
+      hs[kHsL] = fmaf(hs[kHsL], f, la);
+      hs[kHsC0] = fmaf(hs[kHsC0], f2, c0a);
+      hs[kHsC2] = fmaf(hs[kHsC2], f2, c2a);
+      hs[kHsM] = M1;
+      hs[kHsPl] = bl;
+      hs[kHsPk] = __int_as_float(bk);
+      if (bl > -INFINITY) {
+        const float *pe = P.at(bk / kPivMax, hh) + 1 + 3 * (bk % kPivMax);
+        hs[kHsPr] = pe[0];
+        hs[kHsPp] = pe[2];
+      }
+    }
+  }
+  __syncthreads();
+}
+
 template <int GB>
 __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, int64_t cbase,
-                               int nsp, const CandSrc &C, const FinLds<GB> &F) {
+                               int nsp, const CandSrc &C, const PivSrc &P, const FinLds<GB> &F) {
   const int lane = threadIdx.x & 63;
   const int64_t uh0 = (int64_t)u * L.G + h0;
 
-  // (1) yhat, Vhat, ln Nhat: 8 lanes per head, 16 dims per lane.
+  // (1) yhat, Vhat, ln Nhat: 8 lanes per head, 16 dims per lane.  With a pivot p (weight w_p,
+  //     value v_p) outside the rest sums l_r, o_r, C0, Cv, C2:
+  //       l = l_r + w_p,  yhat = (o_r + w_p v_p) / l,  d = yhat - v_p = (o_r - l_r v_p) / l,
+  //       Vhat l^2 = [C2 - 2 yhat.Cv + |yhat|^2 C0] + c_p |d|^2,   c_p = (1 - pi_p) w_p^2,
+  //     where neither the bracket (rest rows only) nor d cancels when the pivot dominates.
   {
     const int h = lane >> 3, j = lane & 7;
-    float yy = 0.0f, ycv = 0.0f;
+    float yy = 0.0f, ycv = 0.0f, dd = 0.0f;
     if (h < GB) {
-      const float il = 1.0f / F.hs[h * kHs + kHsL];
+      const float *hs = F.hs + h * kHs;
+      const float lr = hs[kHsL];
+      const bool piv = hs[kHsPl] > -INFINITY;
+      float wp = 0.0f, vp[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) vp[t] = 0.0f;
+      if (piv) {
+        wp = fast_exp2(hs[kHsPl] - hs[kHsM]);
+        const uint4 *vr = reinterpret_cast<const uint4 *>(
+            L.Vc + (cbase + __float_as_int(hs[kHsPr])) * kHeadDim + 16 * j);
+        const uint4 va = vr[0], vb = vr[1];
+        const uint32_t vw[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          vp[2 * t] = bf16_lo(vw[t]);
+          vp[2 * t + 1] = bf16_hi(vw[t]);
+        }
+      }
+      const float il = 1.0f / (lr + wp);
       float4 *oh = reinterpret_cast<float4 *>(F.o + h * kHeadDim + 16 * j);
       const float4 *cv = reinterpret_cast<const float4 *>(F.o + (GB + h) * kHeadDim + 16 * j);
       float4 *yo = reinterpret_cast<float4 *>(L.y + (uh0 + h) * kHeadDim + 16 * j);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float4 a = oh[q];
-        const float4 b = cv[q];
-        a.x *= il;
-        a.y *= il;
-        a.z *= il;
-        a.w *= il;
-        yy += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
-        ycv += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
-        oh[q] = a;
-        yo[q] = a;
+        const float4 a = oh[q], b = cv[q];
+        const float ov[4] = {a.x, a.y, a.z, a.w}, cvv[4] = {b.x, b.y, b.z, b.w};
+        float yv[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          yv[t] = fmaf(wp, vp[4 * q + t], ov[t]) * il;
+          const float dv = fmaf(-lr, vp[4 * q + t], ov[t]) * il;
+          yy = fmaf(yv[t], yv[t], yy);
+          ycv = fmaf(yv[t], cvv[t], ycv);
+          dd = fmaf(dv, dv, dd);
+        }
+        oh[q] = make_float4(yv[0], yv[1], yv[2], yv[3]);
+        yo[q] = oh[q];
       }
     }
 #pragma unroll
     for (int o = 1; o < 8; o <<= 1) {
       yy += __shfl_xor(yy, o);
       ycv += __shfl_xor(ycv, o);
+      dd += __shfl_xor(dd, o);
     }
     if (h < GB && j == 0) {
       float *hs = F.hs + h * kHs;
-      const float l = hs[kHsL];
-      const float num = hs[kHsC2] - 2.0f * ycv + yy * hs[kHsC0];
+      const bool piv = hs[kHsPl] > -INFINITY;
+      const float wp = piv ? fast_exp2(hs[kHsPl] - hs[kHsM]) : 0.0f;
+      const float pp = piv ? hs[kHsPp] : 1.0f;
+      const float l = hs[kHsL] + wp;
+      const float num = hs[kHsC2] - 2.0f * ycv + yy * hs[kHsC0] + (1.0f - pp) * wp * wp * dd;
       const float sc = sqrtf(hs[kHsC2]) + sqrtf(yy * hs[kHsC0]);
-      const bool redo = num < kCancelFrac * sc * sc;  // never when there is no tail row (sc = 0)
+      const bool redo = num < kCancelFrac * sc * sc;  // never when the rest has no tail row
       const float V = fmaxf(num, 0.0f) / (l * l);
       if (!L.plain && !redo) L.vhat[uh0 + h] = V;
       L.lse[uh0 + h] = hs[kHsM] * kLn2 + logf(l);
+      hs[kHsL] = l;
       hs[kHsYn] = sqrtf(yy);
-      hs[kHsLb] = 0.0f;
+      hs[kHsLb] = piv ? sqrtf(1.0f - pp) * wp * sqrtf(dd) / l : 0.0f;  // the pivot's range term
       hs[kHsV] = V;
       hs[kHsRedo] = redo ? 1.0f : 0.0f;
       F.best[h] = 0ull;
@@ -376,6 +576,38 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
   }
   __syncthreads();
   if (L.plain) return;  // the uncorrected pass only replaces y and ln N
+
+  // (1c) The range terms of the pivot list entries added back in pivot_prepare (they are in no
+  //      candidate list): sqrt(1 - pi) w |v - yhat| / l, exactly.
+  {
+    const int h = lane >> 3, j = lane & 7;
+    const bool act = h < GB;
+    const int hh = act ? h : 0;
+    const float *hs = F.hs + hh * kHs;
+    const int pk = __float_as_int(hs[kHsPk]);
+    const float M = hs[kHsM], il = 1.0f / hs[kHsL];
+    const float *yh = F.o + hh * kHeadDim + 16 * j;
+    float bmax = 0.0f;
+    for_each_pivot(P, nsp, hh, act, [&](int row, float lgt, float p, int key) {
+      if (key == pk) return;
+      const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + row) * kHeadDim + 16 * j);
+      const uint4 va = vr[0], vb = vr[1];
+      const uint32_t vw[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+      float d2 = 0.0f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float a = bf16_lo(vw[t]) - yh[2 * t], b = bf16_hi(vw[t]) - yh[2 * t + 1];
+        d2 = fmaf(a, a, d2);
+        d2 = fmaf(b, b, d2);
+      }
+      d2 += __shfl_xor(d2, 1);
+      d2 += __shfl_xor(d2, 2);
+      d2 += __shfl_xor(d2, 4);
+      bmax = fmaxf(bmax, sqrtf(1.0f - p) * fast_exp2(lgt - M) * sqrtf(d2) * il);
+    });
+    if (act && j == 0) F.hs[h * kHs + kHsLb] = fmaxf(F.hs[h * kHs + kHsLb], bmax);
+    __syncthreads();
+  }
 
   // q of every head into the Cv slots, once Cv is no longer needed (the direct variance sums and
   // the range-term rescans recompute logits).
@@ -481,7 +713,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     }
 #pragma unroll
     for (int o = 1; o < 8; o <<= 1) d2 += __shfl_xor(d2, o);
-    if (have && j == 0) F.hs[h * kHs + kHsLb] = fg * sqrtf(d2);
+    if (have && j == 0) F.hs[h * kHs + kHsLb] = fmaxf(F.hs[h * kHs + kHsLb], fg * sqrtf(d2));
   }
   __syncthreads();
 
@@ -610,12 +842,19 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       const float ai = __uint_as_float(
           ((__float_as_uint(blk[kChAL + (i & 3) / 2 + 2 * (i >> 2)]) >> (16 * (i & 1))) & 0xffffu) << 16);
       const uint64_t lanes = __ballot((lane & 7) == 0 && fk * (ai + bterm) > hs[kHsLb]);
+      // rows in the split's pivot list are in no sum here; their terms were taken in step (1c)
+      const float *plist = P.at(s, h);
+      const int pn = __float_as_int(plist[0]);
       float best = 0.0f;
       for (uint64_t lm = lanes; lm; lm &= lm - 1) {
         const int li = (int)__builtin_ctzll(lm) >> 3;
         if (lane == 0) atomicAdd(diag_of(L, u, h0), 1u);
         const int j = ra + 16 * (lane >> 1) + 4 * (li & 3) + 2 * (li >> 2) + (lane & 1);
         if (j >= rz) continue;
+        bool listed = false;
+#pragma unroll
+        for (int e = 0; e < kPivMax; ++e) listed |= e < pn && __float_as_int(plist[1 + 3 * e]) == j;
+        if (listed) continue;
         const uint4 *kr = reinterpret_cast<const uint4 *>(L.Kc + (cbase + j) * kHeadDim);
         const uint4 *vr = reinterpret_cast<const uint4 *>(L.Vc + (cbase + j) * kHeadDim);
         const float pj = L.pic[cbase + j];
@@ -889,8 +1128,17 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   SplitState S;
 #pragma unroll
   for (int db = 0; db < 8; ++db) S.acc[db] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  S.mrun = active ? -INFINITY : 0.0f;
+  // A finite floor rather than -inf: a split whose only rows are pivots keeps no row in its sums,
+  // and its weights exp2(-inf - floor) are then 0 (exp2(-inf + inf) would be NaN); scale factors
+  // from that floor to any real maximum underflow to 0 as well.
+  S.mrun = active ? -1e30f : 0.0f;
   S.s0 = S.s1 = 0.0f;
+  S.pl = -INFINITY;
+  float *s_piv = s_chunk + L.nchunk * GB * kChunkFloats;  // [GB][kPivFloats]
+  if (isW && g == 0) {  // empty lists
+    s_piv[c * kPivFloats] = __int_as_float(0);
+    s_piv[c * kPivFloats + kPivLogit] = -INFINITY;
+  }
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     S.ck[e] = S.cg[e] = 0.0f;
@@ -917,7 +1165,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   constexpr int kChunkTiles = kChunkRows / 16;
   // tile tt of the split, then the flush of its chunk if tt ends one
   auto step = [&](const Tile &T, int tt) {
-    split_tile(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, plain, scale2);
+    split_tile<(GB > 7)>(S, T, qop, nv0 - 16 * tt, rb0 + 16 * tt, isC, plain, scale2, s_piv, hs, isW);
     if ((tt + 1) % kChunkTiles == 0)
       flush_chunk<GB>(S, s_chunk, tt / kChunkTiles, g, c, row0 + (tt / kChunkTiles) * kChunkRows);
   };
@@ -946,7 +1194,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   if (L.nsplit == 1) {
     // The unit is this one split: its sums go to LDS beside the chunk blocks and the wave
     // finalizes its heads itself (no record, no second launch).
-    FinLds<GB> F(s_chunk + L.nchunk * GB * kChunkFloats);
+    FinLds<GB> F(s_piv + GB * kPivFloats);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int slot = 4 * g + i;
@@ -966,7 +1214,9 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
     if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
     __syncthreads();
     const CandSrc C{s_chunk, 0, GB * kChunkFloats, kChunkFloats};
-    finalize_block<GB>(L, u, h0, cnt, cbase, 1, C, F);
+    const PivSrc P{s_piv, 0, kPivFloats};
+    pivot_prepare<GB>(L, cbase, 1, P, F);
+    finalize_block<GB>(L, u, h0, cnt, cbase, 1, C, P, F);
     return;
   }
   // Several splits: this one's record (sums from registers, chunk blocks from LDS).
@@ -992,7 +1242,9 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
     rec[kRecC0] = s0;
     rec[kRecC2] = s1;
   }
-  __syncthreads();  // the chunk blocks are in LDS
+  __syncthreads();  // the chunk blocks and the pivot lists are in LDS
+  for (int e = lane; e < GB * kPivFloats; e += 64)
+    rec_base[(int64_t)(e / kPivFloats) * L.rec + kRecPiv + e % kPivFloats] = s_piv[e];
   const int nblk = nck * GB * kChunkFloats;
   for (int e = lane; e < nblk; e += 64) {
     const int k = e / (GB * kChunkFloats), r = e % (GB * kChunkFloats);
@@ -1101,7 +1353,9 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
 
   __syncthreads();
   const CandSrc C{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
-  finalize_block<GB>(L, u, h0, cnt, cbase, nsp, C, F);
+  const PivSrc P{rec0 + kRecPiv, sstride, L.rec};
+  pivot_prepare<GB>(L, cbase, nsp, P, F);
+  finalize_block<GB>(L, u, h0, cnt, cbase, nsp, C, P, F);
 }
 
 template <int GB>
@@ -1118,7 +1372,7 @@ size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t spli
 }
 
 size_t attend_split_lds(const AttendLaunch &L, int gb) {
-  size_t b = (size_t)L.nchunk * gb * kChunkFloats * sizeof(float);
+  size_t b = ((size_t)L.nchunk * kChunkFloats + kPivFloats) * gb * sizeof(float);
   if (L.nsplit == 1) {
     size_t f = 0;
     switch (gb) {

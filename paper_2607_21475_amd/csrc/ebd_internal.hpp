@@ -33,6 +33,8 @@ constexpr int kCand = 32;            // candidates per (chunk, head)
 //   [0] m  final running max        [1] l  = sum w        (scale 2^{-m})
 //   [2] C0 = sum c                  [3] C2 = sum c |v|^2  (scale 2^{-2m})
 //   [8..135] o = sum w v            [136..263] Cv = sum c v
+//   [264..291] the split's pivot list: [0] entry count (int bits), then per entry (row as int
+//     bits, base-2 logit, pi); these rows are in none of the sums above nor in any candidate list
 //   then one block of kChunkFloats per chunk of kChunkRows rows:
 //     [0] A  max over the chunk's non-candidates of g |v|   [1] B  ... of g
 //     [2] Vmax  max |v| over the candidates   [3] m_k  running max the block is scaled by
@@ -42,7 +44,10 @@ constexpr int kCand = 32;            // candidates per (chunk, head)
 //     lane i in word i / 2, half i % 2; lane i owns row group i % 4 of the tiles of parity i / 4)
 //   with w = 2^(l2 - m), c = (1 - pi) w^2, g = sqrt(1 - pi) w.
 constexpr int kRecM = 0, kRecL = 1, kRecC0 = 2, kRecC2 = 3, kRecO = 8, kRecCv = 136;
-constexpr int kRecChunks = 264;
+constexpr int kPivMax = 8;      // pivot entries per (split, head)
+constexpr int kPivFloats = 28;  // count, kPivMax x (row, logit, pi), padding to 16 bytes
+constexpr int kRecPiv = 264;
+constexpr int kRecChunks = kRecPiv + kPivFloats;
 constexpr int kChunkFloats = 56;
 constexpr int kChA = 0, kChB = 1, kChVmax = 2, kChM = 3, kChG = 4, kChI = 36, kChAL = 52;
 

@@ -135,8 +135,8 @@ def test_workspace_sizes():
     a.delta = 0.1
     m = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, a)
 
-    def rec(split_rows):  # floats per record: sums, o, Cv, one block per 512-row chunk
-        return 264 + 56 * ((split_rows + 511) // 512)
+    def rec(split_rows):  # floats per record: sums, o, Cv, pivot list, one block per 512-row chunk
+        return 264 + 28 + 56 * ((split_rows + 511) // 512)
 
     def counts(U, G):  # two counts per (unit, block of 8 query heads), 256-byte padded
         return (8 * U * ((G + 7) // 8) + 255) // 256 * 256

@@ -509,26 +509,35 @@ def _dominated_unit(rng, n, G, q, boost, pi_floor=1e-6, tail_pi=(0.05, 1.0)):
     return K, V, pi
 
 
-@pytest.mark.parametrize("G,n,boost,split", [
-    (1, 600, 0.0, 0),     # 1/pi = 1e6 alone: the floor row outweighs the rest of Nhat ~3e2-fold
-    (4, 1500, 4.0, 0),    # its key also aligned with head 0's query: ~7e3-fold for that head
-    (7, 3000, 3.0, 0),
-    (4, 5000, 4.5, 512),  # several splits: the direct sum runs in attend_finalize
-    (8, 900, 2.0, 128),
-    (4, 1500, 9.0, 0),    # 1e5 to 1e7-fold: the floor row alone makes yhat to fp32 precision
+@pytest.mark.parametrize("G,n,boost,split,dup", [
+    (1, 600, 0.0, 0, False),     # 1/pi = 1e6 alone: the floor row outweighs the rest ~3e2-fold
+    (4, 1500, 4.0, 0, False),    # its key also aligned with head 0's query: ~7e3-fold there
+    (7, 3000, 3.0, 0, False),
+    (4, 5000, 4.5, 512, False),  # several splits: pivots from every split meet in attend_finalize
+    (8, 900, 2.0, 128, False),
+    (4, 1500, 9.0, 0, False),    # 1e5 to 1e7-fold: the floor row alone makes yhat to fp32 precision
+    (4, 1500, 4.0, 0, True),     # two identical dominating rows: the direct re-summation
+    (7, 3000, 3.0, 512, True),
 ])
-def test_attend_vhat_cancellation_direct_sum(G, n, boost, split):
-    """A floor row (pi = 1e-6) retained and dominating Nhat: yhat ~ v_j, so C2 - 2 yhat.Cv +
-    |yhat|^2 C0 cancels by many orders of magnitude.  The finalize detects it and sums Vhat
-    directly; Vhat, b and r must match the oracle's two-pass definition."""
-    _say("attend vhat cancellation G=%d n=%d boost=%s split=%d" % (G, n, boost, split))
+def test_attend_vhat_dominant_tail_row(G, n, boost, split, dup):
+    """A floor row (pi = 1e-6) retained and dominating Nhat: yhat ~ v_j, so the one-pass
+    C2 - 2 yhat.Cv + |yhat|^2 C0 would cancel by many orders of magnitude.  The split kernel
+    keeps the largest-weight row of each head out of its sums and the finalize adds it back in
+    closed form, so Vhat, b and r match the oracle's two-pass definition without a second pass.
+    With the dominating row duplicated (two identical rows), the rest sums themselves cancel and
+    the finalize sums those heads again directly."""
+    _say("attend dominant tail row G=%d n=%d boost=%s split=%d dup=%s" % (G, n, boost, split, dup))
     from paper_2607_21475_amd import cache
-    from helpers import rand_bf16
+    from helpers import bf16_to_f64, rand_bf16
 
     rng = np.random.default_rng(100 + G)
     U = 6
     q = rand_bf16(rng, (U, G, 128))
     units = [_dominated_unit(rng, n, G, q[u], boost) for u in range(U - 1)]
+    if dup:  # a copy of the dominating row right after it
+        for K_, V_, p_ in units:
+            j = n // 2
+            K_[j + 1], V_[j + 1], p_[j + 1] = K_[j], V_[j], p_[j]
     units.append((rand_bf16(rng, (n, 128)), rand_bf16(rng, (n, 128)),
                   rng.uniform(0.05, 1.0, n).astype(np.float32)))  # an ordinary unit beside them
     rc = _retained_cache(units)
@@ -536,11 +545,13 @@ def test_attend_vhat_cancellation_direct_sum(G, n, boost, split):
     res = cache.attend_certify(rc, qt, split_rows=split)
     torch.cuda.synchronize()
     ref = _check_attend(rc, res, qt, G)
-    assert cache.direct_variances(res["ws"], U, G) >= U - 1
+    direct = cache.direct_variances(res["ws"], U, G)
+    if dup:
+        assert direct >= U - 1
+    else:
+        assert direct == 0
     # the dominated units really are in the cancelling regime: head 0's Vhat is far below the
-    # scale |v_j|^2 of the dominating row's own C2 term (more than 6 bits cancel)
-    from helpers import bf16_to_f64
-
+    # scale |v_j|^2 of the dominating row's own C2 term (more than 6 bits would cancel)
     vj2 = np.array([np.sum(bf16_to_f64(Vu[n // 2]) ** 2) for _, Vu, _ in units[:U - 1]])
     assert np.all(ref["vhat"][: U - 1, 0] < vj2 / 64)
 
