@@ -82,19 +82,24 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str,
     import statistics
 
     def load(d, counter):
+        """Per library kernel: its readings.  Calibration: the 1 GiB copies and sums that
+        copy_calibration runs after every library kernel (the last dispatches of the run; the
+        inputs' own copies, earlier in the run, are of other sizes)."""
         per, calib, rcal = {}, [], []
+        rows = []
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            for row in csv.DictReader(open(f)):
-                if row["Counter_Name"] != counter:
-                    continue
-                name, v = row["Kernel_Name"], float(row["Counter_Value"])
-                if "ebd::" in name:
-                    k = name.split("(")[0].replace("void ", "").replace("ebd::", "")
-                    k = k.replace("_kernel", "").split("<")[0]
-                    per.setdefault(k, []).append(v)
-                elif "copyBuffer" in name and v > 0.25 * (1 << 20):
+            rows += [r for r in csv.DictReader(open(f)) if r["Counter_Name"] == counter]
+        last_lib = max((int(r["Dispatch_Id"]) for r in rows if "ebd::" in r["Kernel_Name"]), default=-1)
+        for r in rows:
+            name, v = r["Kernel_Name"], float(r["Counter_Value"])
+            if "ebd::" in name:
+                k = name.split("(")[0].replace("void ", "").replace("ebd::", "")
+                k = k.replace("_kernel", "").split("<")[0]
+                per.setdefault(k, []).append(v)
+            elif int(r["Dispatch_Id"]) > last_lib and v > 0.25 * (1 << 20):
+                if "copyBuffer" in name:
                     calib.append(v)  # the 1 GiB calibration copies
-                elif "reduce" in name and v > 0.25 * (1 << 20):
+                elif "reduce" in name:
                     rcal.append(v)  # the 1 GiB read-only calibration sums
         return per, calib, rcal
 

@@ -22,23 +22,28 @@ def test_more_than_one_gpu_exits_with_a_message():
 def _write_counters(d, counter, rows):
     os.makedirs(d, exist_ok=True)
     with open(os.path.join(d, "pmc_counter_collection.csv"), "w", newline="") as f:
-        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
         w.writeheader()
-        for name, v in rows:
-            w.writerow({"Kernel_Name": name, "Counter_Name": counter, "Counter_Value": v})
+        for i, (name, v) in enumerate(rows):
+            w.writerow({"Dispatch_Id": i + 1, "Kernel_Name": name, "Counter_Name": counter,
+                        "Counter_Value": v})
 
 
 def test_counter_summary_scales_by_the_calibration_copy(tmp_path):
     gib_kib = float(1 << 20)
-    # the counters read half the copy's fetched bytes and all of its written bytes
-    fetch_rows = [("__amd_rocclr_copyBuffer", gib_kib / 2), ("__amd_rocclr_copyBuffer", 4.0),
+    # the counters read half the copy's fetched bytes and all of its written bytes; an input copy
+    # of 4 GiB before the library's kernels is not a calibration copy
+    fetch_rows = [("__amd_rocclr_copyBuffer", 2 * gib_kib),
                   ("ebd::evict_copy_kernel(ebd::EvictLaunch)", 1000.0),
                   ("ebd::evict_copy_kernel(ebd::EvictLaunch)", 3000.0),
-                  ("void ebd::attend_split_kernel<7>(ebd::AttendLaunch, int)", 500.0)]
-    write_rows = [("__amd_rocclr_copyBuffer", gib_kib),
+                  ("void ebd::attend_split_kernel<7>(ebd::AttendLaunch, int)", 500.0),
+                  ("__amd_rocclr_copyBuffer", gib_kib / 2), ("__amd_rocclr_copyBuffer", 4.0),
+                  ("void at::native::reduce_kernel<512, 1>", gib_kib / 2)]
+    write_rows = [("__amd_rocclr_copyBuffer", 4 * gib_kib),
                   ("ebd::evict_copy_kernel(ebd::EvictLaunch)", 2000.0),
                   ("ebd::evict_copy_kernel(ebd::EvictLaunch)", 2000.0),
-                  ("void ebd::attend_split_kernel<7>(ebd::AttendLaunch, int)", 10.0)]
+                  ("void ebd::attend_split_kernel<7>(ebd::AttendLaunch, int)", 10.0),
+                  ("__amd_rocclr_copyBuffer", gib_kib)]
     _write_counters(str(tmp_path / "f"), "FETCH_SIZE", fetch_rows)
     _write_counters(str(tmp_path / "w"), "WRITE_SIZE", write_rows)
     out = str(tmp_path / "out")
@@ -46,6 +51,7 @@ def test_counter_summary_scales_by_the_calibration_copy(tmp_path):
                                out_dir=out) == 0
     rec = json.load(open(os.path.join(out, "hbm_traffic_unit_test.json")))
     assert abs(rec["fetch_scale"] - 2.0) < 1e-12 and abs(rec["write_scale"] - 1.0) < 1e-12
+    assert abs(rec["fetch_scale_read_only_sum"] - 2.0) < 1e-12
     k = rec["kernels"]["evict_copy"]
     assert k["fetch_bytes_per_launch"] == 2 * 2000 * 1024  # mean 2000 KiB, scaled by 2
     assert k["write_bytes_per_launch"] == 2000 * 1024
@@ -55,11 +61,11 @@ def test_counter_summary_scales_by_the_calibration_copy(tmp_path):
 
 
 def test_committed_traffic_is_used_only_while_the_sources_match():
-    path = os.path.join(ROOT, "profiles", "hbm_traffic_qwen7b_6k.json")
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b_16k.json")
     rec = json.load(open(path))
-    got = bench.load_traffic("qwen7b_6k", "evict_copy")
+    got = bench.load_traffic("llama8b_16k", "attend_split")
     if rec["kernel_sources_hash"] == bench.kernel_sources_hash():
-        assert got == rec["kernels"]["evict_copy"]["bytes_per_launch"]
+        assert got == rec["kernels"]["attend_split"]["bytes_per_launch"]
     else:
         assert got is None
     assert bench.load_traffic("no_such_workload", "evict_copy") is None
