@@ -167,6 +167,12 @@ def main() -> int:
     ap.add_argument("--compare-units", type=int, default=256)
     ap.add_argument("--next-steps", type=int, default=3,
                     help="timed repetitions of the rows built after the hot path (0: skip)")
+    ap.add_argument("--replay-grid", action="store_true",
+                    help="instead of the legs: the whole replay grid (12096 cells x 8 KV heads, "
+                         "G = 1), evicted chunk by chunk, certified in one launch, with coverage "
+                         "of the full-cache error per (budget, context)")
+    ap.add_argument("--replay-chunks", type=int, default=8,
+                    help="chunks the replay grid's full caches are generated and evicted in")
     ap.add_argument("--replay-chunk", type=int, default=-1, metavar="CHUNK",
                     help="instead of a workload: time one chunk (0..7) of 1512 cells of the replay "
                          "grid (8 KV heads per cell, G = 1, per-unit budgets and contexts)")
@@ -195,6 +201,8 @@ def main() -> int:
         return compare_arms(args, wl, budgets)
     if args.replay_chunk >= 0:
         return replay_chunk(args)
+    if args.replay_grid:
+        return replay_grid(args)
 
     names = [args.workload] if args.workload else [w for w in args.legs.split(",") if w]
     legs = {}
@@ -676,6 +684,148 @@ def next_rows(args, wl, inp, plans, ebd, torch):
     ebd.ebd_timing_enable(False)
     res["designs"] = designs
     return res
+
+
+def replay_grid(args) -> int:
+    """The whole replay grid: 12096 cells x 8 KV heads = 96768 units (G = 1), cell c with budget
+    5/10/15/25/50% (c mod 5) and context 2048/6144/16384 ((c div 5) mod 3).  Their full caches
+    (406 GB) exceed the GPU's memory, so they are generated and evicted chunk by chunk into one
+    compacted cache of all units; while a chunk's full cache is resident, its full-cache output
+    y (eq. (1)) is computed by the certified kernel itself over the uncompacted rows with pi = 1
+    (the Hajek output then is eq. (1), and the certificate is 0).  Then one certified step over
+    all 96768 units (one launch per kernel) gives yhat and the radius r, and coverage
+    |yhat - y| / |y| <= r, the median error and radius and the Spearman correlation of radius and
+    error are reported per (budget, context).  Timed: the chunk evictions (HIP events) and the
+    all-unit certified step (args.steps repetitions)."""
+    import torch
+
+    import synth
+    import paper_2607_21475_amd as ebd
+    from paper_2607_21475_amd import cache
+
+    H = synth.REPLAY_KV_HEADS
+    ncell = synth.REPLAY_CELLS
+    cells = [synth.replay_cell(c) for c in range(ncell)]
+    lengths = [ctx for (_, ctx, _, _) in cells for _ in range(H)]
+    budgets = [b for (b, _, _, _) in cells for _ in range(H)]
+    U = len(lengths)
+    t0 = time.time()
+    cap_host = cache.plan_capacity(lengths, budgets, 4, 64, pi_min=0.01)
+    rc = _alloc_retained(torch, cache, cap_host, U)
+    q = synth.make_queries(U, 1, seed=args.seed + 7, device="cuda")
+    bpu = torch.tensor(budgets, dtype=torch.float32, device="cuda")
+    yfull = torch.empty((U, 1, 128), dtype=torch.float32, device="cuda")
+    per = -(-ncell // args.replay_chunks)
+    ev_ms, ev_calls, full_rows = 0.0, 0, 0
+    for k in range(args.replay_chunks):
+        c0, c1 = k * per, min(ncell, (k + 1) * per)
+        if c0 >= c1:
+            break
+        u0, u1 = c0 * H, c1 * H
+        lens = lengths[u0:u1]
+        Uc = u1 - u0
+        K, V, seq_off = synth.make_cache(lens, seed=args.seed + 100 + k, device="cuda")
+        sc = synth.window_scores(K, seq_off, seed=args.seed + 200 + k)
+        r0, r1 = cap_host[u0], cap_host[u1]
+        coff = torch.tensor([x - r0 for x in cap_host[u0:u1 + 1]], dtype=torch.int64, device="cuda")
+        maxcap = max(cap_host[i + 1] - cap_host[i] for i in range(u0, u1))
+        ep = ebd.evict_params(Uc, max(lens), maxcap, seq_off, coff, 4, 64, 0.0, bpu[u0:u1], 0.01, 0,
+                              args.seed + k, None, 0)
+        ews = ebd.workspace(ebd.ebd_workspace_size(ebd.EBD_WS_EVICT, ep))
+
+        def evict():
+            ebd.ebd_evict(ep, sc, K, V, rc.Kc[r0:r1], rc.Vc[r0:r1], rc.pic[r0:r1], rc.idxc[r0:r1],
+                          rc.count[u0:u1], rc.status[u0:u1], ews)
+
+        evict()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            evict()
+        e1.record()
+        # full-cache reference output: every row kept with pi = 1
+        ones = torch.ones((K.shape[0],), dtype=torch.float32, device="cuda")
+        nfull = torch.tensor(lens, dtype=torch.int32, device="cuda")
+        fp = ebd.attend_params(Uc, 1, max(lens), seq_off)
+        fws = ebd.workspace(ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, fp))
+        scratch = _outputs(torch, Uc, 1)
+        ebd.ebd_attend_certify(fp, q[u0:u1], K, V, ones, nfull, yfull[u0:u1], scratch["vhat"],
+                               scratch["lse"], fws)
+        torch.cuda.synchronize()
+        ev_ms += e0.elapsed_time(e1)
+        ev_calls += args.steps
+        full_rows += int(K.shape[0])
+        print("replay grid: chunk %d cells %d..%d, %d units, %.1f GB of full cache (%.0f s)"
+              % (k, c0, c1, Uc, 512 * K.shape[0] / 1e9, time.time() - t0), file=sys.stderr, flush=True)
+        del K, V, seq_off, sc, ones, nfull, fws, scratch, ews
+        torch.cuda.empty_cache()
+    if (rc.status.cpu().numpy() & ebd.EBD_ST_CAP_OVERFLOW).any():
+        raise RuntimeError("capacity overflow in the replay grid")
+    retained = int(rc.count.sum().item())
+
+    # one certified step over every unit
+    ap_ = ebd.attend_params(U, 1, rc.max_cap, rc.cap_off)
+    aws = ebd.workspace(ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, ap_))
+    o = _outputs(torch, U, 1)
+    ast = torch.empty((U,), dtype=torch.int32, device="cuda")
+
+    def attend():
+        ebd.ebd_attend_certify(ap_, q, rc.Kc, rc.Vc, rc.pic, rc.count, o["y"], o["vhat"], o["lse"],
+                               aws, brange=o["b"], radius=o["r"], status=ast)
+
+    attend()
+    torch.cuda.synchronize()
+    ebd.ebd_timing_enable(True)
+    for k in ("attend_split", "attend_finalize"):
+        ebd.ebd_timing_read(k)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        attend()
+    e1.record()
+    torch.cuda.synchronize()
+    kt = {k: ebd.ebd_timing_read(k) for k in ("attend_split", "attend_finalize")}
+    ebd.ebd_timing_enable(False)
+    att_ms = e0.elapsed_time(e1) / args.steps
+    if ast.cpu().numpy().any():
+        raise RuntimeError("rows the certified step could not see")
+
+    # coverage of the full-cache error, per (budget, context)
+    err = (torch.linalg.norm(o["y"] - yfull, dim=2) / torch.linalg.norm(yfull, dim=2)).flatten()
+    r = o["r"].flatten()
+    cell_of = torch.arange(U, device="cuda") // H
+    bi, ci = cell_of % 5, (cell_of // 5) % 3
+    table = []
+    for b in range(5):
+        for c in range(3):
+            m = (bi == b) & (ci == c)
+            e_, r_ = err[m], r[m]
+            table.append({"budget": synth.REPLAY_BUDGETS[b], "context": synth.REPLAY_CONTEXTS[c],
+                          "units": int(m.sum()),
+                          "coverage": round(float((e_ <= r_).float().mean()), 4),
+                          "median_rel_err": float("%.4g" % float(e_.median())),
+                          "median_radius": float("%.4g" % float(r_.median())),
+                          "spearman_radius_error": round(_spearman(r_, e_), 4)})
+    kv = 512 * retained
+    line = {"mode": "replay_grid", "cells": ncell, "units": U, "group": 1,
+            "full_cache_rows": full_rows, "full_cache_gb": round(512 * full_rows / 1e9, 1),
+            "retained_rows": retained, "retained_kv_gb": round(kv / 1e9, 2),
+            "chunks": args.replay_chunks, "steps": args.steps,
+            "evict_ms_per_pass": round(ev_ms / ev_calls * args.replay_chunks, 3),
+            "evictions_per_s": round(U * ev_calls / args.replay_chunks / (ev_ms * 1e-3), 1),
+            "evict_gbs": round((4 * full_rows + 1032 * retained) * ev_calls / args.replay_chunks
+                               / (ev_ms * 1e-3) / 1e9, 1),
+            "attend_ms": round(att_ms, 3),
+            "attend_launches_per_step": {k: kt[k][1] // args.steps for k in kt},
+            "attend_kernel_ms": {k: round(kt[k][0] / max(kt[k][1], 1), 3) for k in kt},
+            "retained_kv_gbs": round(kv / (att_ms * 1e-3) / 1e9, 1),
+            "retained_kv_frac_hbm": round(kv / (att_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "coverage_all": round(float((err <= r).float().mean()), 4),
+            "per_budget_context": table,
+            "data": "synthetic caches in the replay grid's shapes (the paper's models and prompts "
+                    "are not used); coverage is reported, not gated"}
+    print(json.dumps(line), flush=True)
+    return 0
 
 
 def replay_chunk(args) -> int:
