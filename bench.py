@@ -347,7 +347,6 @@ def decode_leg(wl, args, headline: bool):
     apar = ebd.attend_params(U, G, rc.max_cap, rc.cap_off)
     aws_bytes = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, apar)
     aws = ebd.workspace(aws_bytes)
-    fused = cache.fused_finalize(aws_bytes, U, G)
     o = _outputs(torch, U, G)
     ast = torch.empty((U,), dtype=torch.int32, device="cuda")
     # decode-step inputs: a query block, a new key/value row and its position per step
@@ -408,6 +407,7 @@ def decode_leg(wl, args, headline: bool):
     value = kv_step * K / (decode_ms * 1e-3) / 1e9
     att_rows = T * rows0 + U * T * (T + 1) // 2  # summed over the decode steps of one step
     gathers = kt["evict_copy"][1] == 0
+    fused = kt["attend_finalize"][1] == 0  # the split kernel finalized every unit itself
     alg = {
         "evict_select": 4 * U * n + 8 * rows0 + (1024 * rows0 if gathers else 0),
         "evict_copy": 0 if gathers else 1024 * rows0,
@@ -488,7 +488,7 @@ def budgets_leg(wl, args, headline: bool):
         ap_ = ebd.attend_params(U, G, rc.max_cap, rc.cap_off)
         aws_bytes = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, ap_)
         plans.append(dict(budget=b, rc=rc, ep=ep, ews=ews, ap=ap_, aws=ebd.workspace(aws_bytes),
-                          out=_outputs(torch, U, G), fused=cache.fused_finalize(aws_bytes, U, G)))
+                          out=_outputs(torch, U, G)))
 
     def evict_all():
         for p in plans:
@@ -514,6 +514,13 @@ def budgets_leg(wl, args, headline: bool):
                       rc.count, rc.status, p["ews"])
         torch.cuda.synchronize()
         p["gathers"] = ebd.ebd_timing_read("evict_copy")[1] == 0
+        # ... and whose attention finalizes inside the split kernel (no attend_finalize launch)
+        ebd.ebd_timing_read("attend_finalize")
+        o = p["out"]
+        ebd.ebd_attend_certify(p["ap"], inp["q"], rc.Kc, rc.Vc, rc.pic, rc.count, o["y"],
+                               o["vhat"], o["lse"], p["aws"], brange=o["b"], radius=o["r"])
+        torch.cuda.synchronize()
+        p["fused"] = ebd.ebd_timing_read("attend_finalize")[1] == 0
     for p in plans:
         if (p["rc"].status.cpu().numpy() & ebd.EBD_ST_CAP_OVERFLOW).any():
             raise RuntimeError("capacity overflow at budget %s" % p["budget"])

@@ -159,8 +159,9 @@ def direct_variances(ws: torch.Tensor, num_units: int, group: int) -> int:
     return int(_diag(ws, num_units, group)[:, 1].sum().item())
 
 
-def fused_finalize(ws_bytes: int, num_units: int, group: int) -> bool:
-    """Whether an attention launch planned with this workspace size finalizes inside its split
-    kernel (every unit is one split: the workspace holds only the diagnostic counts)."""
+def uses_split_records(ws_bytes: int, num_units: int, group: int) -> bool:
+    """Whether an attention launch planned with this workspace size cuts units into several
+    splits whose partial records go through the workspace (otherwise it holds only the
+    diagnostic counts)."""
     nhb = (int(group) + 7) // 8
-    return ws_bytes <= (8 * num_units * nhb + 255) // 256 * 256
+    return ws_bytes > (8 * num_units * nhb + 255) // 256 * 256

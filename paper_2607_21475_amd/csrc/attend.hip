@@ -399,13 +399,13 @@ __device__ __forceinline__ void for_each_pivot(const PivSrc &P, int nsp, int h, 
 // rescaled), and every other entry is added back into l, o, C0, Cv, C2 exactly.  8 lanes per
 // head, 16 dims per lane.
 template <int GB>
-__device__ void pivot_prepare(const AttendLaunch &L, int64_t cbase, int nsp, const PivSrc &P,
+__device__ __forceinline__ void pivot_prepare(const AttendLaunch &L, int64_t cbase, int nsp, const PivSrc &P,
                               const FinLds<GB> &F) {
   const int lane = threadIdx.x & 63;
   const int h = lane >> 3, j = lane & 7;
   const bool act = h < GB;
   const int hh = act ? h : 0;
-  __syncthreads();  // the sums are in LDS
+  wave_sync();  // the sums are in LDS
   // the pivot: lanes of a head look at every eighth split, then compare
   float bl = -INFINITY;
   int bk = 0x7fffffff;
@@ -468,7 +468,7 @@ __device__ void pivot_prepare(const AttendLaunch &L, int64_t cbase, int nsp, con
     c0a += cc;
     c2a = fmaf(cc, nv, c2a);
   });
-  __syncthreads();  // every lane has read the sums it rescales
+  wave_sync();  // every lane has read the sums it rescales
   if (act) {
     float4 *op = reinterpret_cast<float4 *>(F.o + hh * kHeadDim + 16 * j);
     float4 *cp = reinterpret_cast<float4 *>(F.o + (GB + hh) * kHeadDim + 16 * j);
@@ -491,11 +491,11 @@ __device__ void pivot_prepare(const AttendLaunch &L, int64_t cbase, int nsp, con
       }
     }
   }
-  __syncthreads();
+  wave_sync();
 }
 
 template <int GB>
-__device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, int64_t cbase,
+__device__ __forceinline__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, int64_t cbase,
                                int nsp, const CandSrc &C, const PivSrc &P, const FinLds<GB> &F) {
   const int lane = threadIdx.x & 63;
   const int64_t uh0 = (int64_t)u * L.G + h0;
@@ -574,7 +574,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       F.best[h] = 0ull;
     }
   }
-  __syncthreads();
+  wave_sync();
   if (L.plain) return;  // the uncorrected pass only replaces y and ln N
 
   // (1c) The range terms of the pivot list entries added back in pivot_prepare (they are in no
@@ -606,7 +606,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       bmax = fmaxf(bmax, sqrtf(1.0f - p) * fast_exp2(lgt - M) * sqrtf(d2) * il);
     });
     if (act && j == 0) F.hs[h * kHs + kHsLb] = fmaxf(F.hs[h * kHs + kHsLb], bmax);
-    __syncthreads();
+    wave_sync();
   }
 
   // q of every head into the Cv slots, once Cv is no longer needed (the direct variance sums and
@@ -620,7 +620,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       F.o[(GB + h) * kHeadDim + 2 * d2] = bf16_lo(qw);
       F.o[(GB + h) * kHeadDim + 2 * d2 + 1] = bf16_hi(qw);
     }
-    __syncthreads();
+    wave_sync();
     qloaded = true;
   };
 
@@ -683,7 +683,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
                                   (unsigned)((x0 + lane) * kCand + jmax));
     }
   }
-  __syncthreads();
+  wave_sync();
 
   // (3) The most promising candidate of every head, 8 lanes per head.
   {
@@ -715,12 +715,12 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
     for (int o = 1; o < 8; o <<= 1) d2 += __shfl_xor(d2, o);
     if (have && j == 0) F.hs[h * kHs + kHsLb] = fmaxf(F.hs[h * kHs + kHsLb], fg * sqrtf(d2));
   }
-  __syncthreads();
+  wave_sync();
 
   // (4) Every other candidate whose bound exceeds its head's best value: listed, then evaluated
   //     sixteen at a time (four lanes per value row).
   auto eval_list = [&](int n) {
-    __syncthreads();  // the list is in LDS
+    wave_sync();  // the list is in LDS
     const int t4 = lane & 3;  // four lanes per candidate, 32 dims each
     for (int i0 = 0; i0 < n; i0 += 16) {
       const int i = i0 + (lane >> 2);
@@ -751,7 +751,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       if (have && t4 == 0)
         atomicMax(reinterpret_cast<unsigned *>(F.hs + h * kHs + kHsLb), __float_as_uint(fg * sqrtf(d2)));
     }
-    __syncthreads();
+    wave_sync();
   };
   // One lane per block marks the candidates whose bound, with a relative margin for rounding,
   // exceeds the head's best value; a wave scan of the counts places them in the list.
@@ -888,7 +888,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       }
       best = wave_max(best) / hs[kHsL];
       if (lane == 0) F.hs[h * kHs + kHsLb] = fmaxf(F.hs[h * kHs + kHsLb], best);
-      __syncthreads();
+      wave_sync();
     }
   }
 
@@ -1055,7 +1055,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
       }
     }
     if (lane == 0) diag_of(L, u, h0)[1] = (uint32_t)__popc(redo);
-    __syncthreads();
+    wave_sync();
   }
 
   // (6) b and the radius of eq. (4).
@@ -1070,7 +1070,7 @@ __device__ void finalize_block(const AttendLaunch &L, int u, int h0, int cnt, in
 
 // Outputs of a unit with no retained rows.
 template <int GB>
-__device__ void finalize_empty(const AttendLaunch &L, int u, int h0) {
+__device__ __forceinline__ void finalize_empty(const AttendLaunch &L, int u, int h0) {
   const int lane = threadIdx.x & 63;
   const int64_t uh0 = (int64_t)u * L.G + h0;
   for (int e = lane; e < GB * kHeadDim; e += 64) L.y[uh0 * kHeadDim + e] = 0.0f;
@@ -1085,16 +1085,35 @@ __device__ void finalize_empty(const AttendLaunch &L, int u, int h0) {
   if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
 }
 
+template <int GB>
+__device__ __forceinline__ void finalize_records(const AttendLaunch &L, int u, int h0, float *s_fin);
+
 // One wave per (unit, split, head block).  Lane (g, c): MFMA column c is head slot c (weights for
 // c < GB, variance weights for GB <= c < 2 GB, idle above); g selects the row group.
-template <int GB>
-__global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int h0) {
-  extern __shared__ float s_chunk[];  // [nchunk][GB][kChunkFloats]
+// Work-groups: one wave each (L.wpg = 1; units of several splits are then finalized by
+// attend_finalize), or, when a unit is cut into L.wpg = L.nsplit splits, the unit's splits as the
+// waves of one work-group: each writes its split record, counts itself in an LDS word, and the
+// wave that arrives last finalizes the unit from the records (no second launch).  Waves of empty
+// splits leave at once; the only work-group barrier is the one after the counter is cleared,
+// which every wave reaches.
+template <int GB, bool COOP>
+__global__ __launch_bounds__(COOP ? 64 * kCoopMaxSplits : 64, 2) void attend_split_kernel(
+    AttendLaunch L, int h0) {
+  extern __shared__ float s_lds[];
   const int bid = blockIdx.x;
-  const int sp = bid % L.nsplit;
-  const int u = bid / L.nsplit;
-  const int lane = threadIdx.x;
+  const int wave = COOP ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0;
+  constexpr bool coop = COOP;
+  const int sp = coop ? wave : bid % L.nsplit;
+  const int u = coop ? bid : bid / L.nsplit;
+  const int lane = threadIdx.x & 63;
   const int g = lane >> 4, c = lane & 15;
+  // this wave's LDS: [nchunk][GB][kChunkFloats] chunk blocks, then [GB][kPivFloats] pivot lists
+  float *s_chunk = s_lds + (coop ? (size_t)wave * (L.nchunk * kChunkFloats + kPivFloats) * GB : 0);
+  int *s_arrived = reinterpret_cast<int *>(s_lds + L.coop_counter);
+  if (coop) {
+    if (threadIdx.x == 0) *s_arrived = 0;
+    __syncthreads();  // before any wave can leave or arrive
+  }
   const int64_t cbase = L.cap_off[u];
   const int64_t cap = L.cap_off[u + 1] - cbase;
   const int64_t held = min((int64_t)L.count[u], cap);
@@ -1104,7 +1123,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
                   (held > (int64_t)cnt ? EBD_ST_BAD_LAYOUT : 0u);
   const int row0 = sp * L.split_rows;
   if (row0 >= cnt) {  // empty split: the finalize skips it; an empty unit gets empty outputs
-    if (L.nsplit == 1) finalize_empty<GB>(L, u, h0);
+    if (sp == 0 && (COOP || L.nsplit == 1)) finalize_empty<GB>(L, u, h0);
     return;
   }
   const int nrow = min(cnt - row0, L.split_rows);
@@ -1191,7 +1210,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
   s0 += __shfl_xor(s0, 32);
   s1 += __shfl_xor(s1, 16);
   s1 += __shfl_xor(s1, 32);
-  if (L.nsplit == 1) {
+  if (!COOP && L.nsplit == 1) {
     // The unit is this one split: its sums go to LDS beside the chunk blocks and the wave
     // finalizes its heads itself (no record, no second launch).
     FinLds<GB> F(s_piv + GB * kPivFloats);
@@ -1212,7 +1231,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
       F.hs[(c - GB) * kHs + kHsC2] = s1;
     }
     if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
-    __syncthreads();
+    wave_sync();
     const CandSrc C{s_chunk, 0, GB * kChunkFloats, kChunkFloats};
     const PivSrc P{s_piv, 0, kPivFloats};
     pivot_prepare<GB>(L, cbase, 1, P, F);
@@ -1242,7 +1261,7 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
     rec[kRecC0] = s0;
     rec[kRecC2] = s1;
   }
-  __syncthreads();  // the chunk blocks and the pivot lists are in LDS
+  wave_sync();  // the chunk blocks and the pivot lists are in LDS
   for (int e = lane; e < GB * kPivFloats; e += 64)
     rec_base[(int64_t)(e / kPivFloats) * L.rec + kRecPiv + e % kPivFloats] = s_piv[e];
   const int nblk = nck * GB * kChunkFloats;
@@ -1251,6 +1270,19 @@ __global__ __launch_bounds__(64, 2) void attend_split_kernel(AttendLaunch L, int
     const int hh = r / kChunkFloats, j = r % kChunkFloats;
     rec_base[(int64_t)hh * L.rec + kRecChunks + k * kChunkFloats + j] = s_chunk[e];
   }
+  if (!COOP) return;
+  // The record is complete (the release makes it visible to the work-group's other waves before
+  // the count moves); the last of the unit's nsp waves to arrive finalizes.  Its FinLds reuses
+  // the LDS of the splits, whose waves are all done with it by then.
+  const int nsp = (cnt + L.split_rows - 1) / L.split_rows;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  int before = 0;
+  if (lane == 0) before = __hip_atomic_fetch_add(s_arrived, 1, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
+  before = __builtin_amdgcn_readfirstlane(before);
+  if (before != nsp - 1) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  finalize_records<GB>(L, u, h0, s_lds);
 }
 
 // attend_finalize: one wave per (unit, head block) when units are cut into several splits.  The
@@ -1264,12 +1296,11 @@ __host__ __device__ constexpr size_t fin_scale_off() {
   return FinLds<GB>::bytes() / sizeof(float);
 }
 
+// The finalize of unit u from its split records, by one wave (s_fin: FinLds, then the split
+// scale factors).
 template <int GB>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
-void attend_finalize_kernel(AttendLaunch L, int h0) {
-  extern __shared__ float s_fin[];  // FinLds, then the split scale factors
-  const int u = blockIdx.x;
-  const int lane = threadIdx.x;
+__device__ __forceinline__ void finalize_records(const AttendLaunch &L, int u, int h0, float *s_fin) {
+  const int lane = threadIdx.x & 63;
   const int64_t cbase = L.cap_off[u];
   const int64_t cap = L.cap_off[u + 1] - cbase;
   const int cnt = (int)min(min((int64_t)L.count[u], cap), (int64_t)L.nsplit * L.split_rows);
@@ -1278,7 +1309,7 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
     return;
   }
   if (lane == 0 && !L.plain) diag_of(L, u, h0)[0] = diag_of(L, u, h0)[1] = 0u;
-  __syncthreads();  // the zeroed words are in place before the finalize's own updates
+  wave_sync();  // the zeroed words are in place before the finalize's own updates
   const int nsp = (cnt + L.split_rows - 1) / L.split_rows;
   const float *rec0 = L.part + ((int64_t)u * L.nsplit * L.G + h0) * L.rec;  // (s, h) at s G rec + h rec
   const int64_t sstride = (int64_t)L.G * L.rec;
@@ -1308,12 +1339,12 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
         F.hs[h * kHs + kHsC0] = c0 + (s0 == 0 ? 0.0f : fo * fo * F.hs[h * kHs + kHsC0]);
         F.hs[h * kHs + kHsC2] = c2 + (s0 == 0 ? 0.0f : fo * fo * F.hs[h * kHs + kHsC2]);
       }
-      __syncthreads();
+      wave_sync();
     }
   }
   // the scale of every split to the combined max
   for (int e = lane; e < nsp * GB; e += 64) fsc[e] = scale_of(fsc[e], F.hs[(e % GB) * kHs + kHsM]);
-  __syncthreads();
+  wave_sync();
 
   // o and Cv: two dims per lane, every slot of SP splits in flight at once.
   {
@@ -1351,11 +1382,18 @@ void attend_finalize_kernel(AttendLaunch L, int h0) {
       reinterpret_cast<float2 *>(F.o + slot * kHeadDim)[lane] = acc[slot];
   }
 
-  __syncthreads();
+  wave_sync();
   const CandSrc C{rec0 + kRecChunks, sstride, kChunkFloats, L.rec};
   const PivSrc P{rec0 + kRecPiv, sstride, L.rec};
   pivot_prepare<GB>(L, cbase, nsp, P, F);
   finalize_block<GB>(L, u, h0, cnt, cbase, nsp, C, P, F);
+}
+
+template <int GB>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void attend_finalize_kernel(AttendLaunch L, int h0) {
+  extern __shared__ float s_fin[];
+  finalize_records<GB>(L, blockIdx.x, h0, s_fin);
 }
 
 template <int GB>
@@ -1371,8 +1409,31 @@ size_t attend_workspace_bytes(int32_t U, int32_t nsplit, int32_t G, int32_t spli
                     sizeof(float);
 }
 
+size_t attend_finalize_lds_gb(const AttendLaunch &L, int gb) {
+  switch (gb) {
+    case 1: return attend_finalize_lds<1>(L);
+    case 2: return attend_finalize_lds<2>(L);
+    case 3: return attend_finalize_lds<3>(L);
+    case 4: return attend_finalize_lds<4>(L);
+    case 5: return attend_finalize_lds<5>(L);
+    case 6: return attend_finalize_lds<6>(L);
+    case 7: return attend_finalize_lds<7>(L);
+    default: return attend_finalize_lds<8>(L);
+  }
+}
+
+// Float offset of the arrival count of a work-group of a unit's splits: after the splits' own
+// LDS and after the finalize's, which reuses the splits' space.
+int32_t attend_coop_counter(const AttendLaunch &L, int gb) {
+  const size_t part = ((size_t)L.nchunk * kChunkFloats + kPivFloats) * gb;
+  const size_t fin = attend_finalize_lds_gb(L, gb) / sizeof(float);
+  const size_t need = part * (size_t)L.wpg > fin ? part * (size_t)L.wpg : fin;
+  return (int32_t)((need + 3) / 4 * 4);
+}
+
 size_t attend_split_lds(const AttendLaunch &L, int gb) {
   size_t b = ((size_t)L.nchunk * kChunkFloats + kPivFloats) * gb * sizeof(float);
+  if (L.nsplit > 1 && L.wpg > 1) return ((size_t)attend_coop_counter(L, gb) + 4) * sizeof(float);
   if (L.nsplit == 1) {
     size_t f = 0;
     switch (gb) {
@@ -1393,6 +1454,7 @@ size_t attend_split_lds(const AttendLaunch &L, int gb) {
 size_t attend_fused_lds_bytes(int32_t split_rows, int gb) {
   AttendLaunch L{};
   L.nsplit = 1;
+  L.wpg = 1;
   L.nchunk = attend_chunks(split_rows);
   return attend_split_lds(L, gb);
 }
@@ -1400,24 +1462,44 @@ size_t attend_fused_lds_bytes(int32_t split_rows, int gb) {
 size_t attend_part_lds_bytes(int32_t split_rows, int gb) {
   AttendLaunch L{};
   L.nsplit = 2;
+  L.wpg = 1;
   L.nchunk = attend_chunks(split_rows);
   return attend_split_lds(L, gb);
 }
 
-hipError_t launch_attend_split(const AttendLaunch &L, hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)L.U * L.nsplit)), block(kAttendThreads);
-  for (int h0 = 0; h0 < L.G; h0 += kHeadBlock) {
-    const int gb = min(kHeadBlock, L.G - h0);
+hipError_t launch_attend_split(const AttendLaunch &L0, hipStream_t s) {
+  if (L0.wpg != 1 && (L0.wpg != L0.nsplit || L0.wpg > kCoopMaxSplits)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((int64_t)L0.U * (L0.wpg > 1 ? 1 : L0.nsplit))),
+      block(kAttendThreads * L0.wpg);
+  for (int h0 = 0; h0 < L0.G; h0 += kHeadBlock) {
+    const int gb = min(kHeadBlock, L0.G - h0);
+    AttendLaunch L = L0;
+    L.coop_counter = L.wpg > 1 ? attend_coop_counter(L, gb) : 0;
     const size_t lds = attend_split_lds(L, gb);
+    const bool coop = L.wpg > 1;
+    if (coop && gb > kCoopMaxHeads) return hipErrorInvalidValue;
     switch (gb) {
-      case 1: hipLaunchKernelGGL(attend_split_kernel<1>, grid, block, lds, s, L, h0); break;
-      case 2: hipLaunchKernelGGL(attend_split_kernel<2>, grid, block, lds, s, L, h0); break;
-      case 3: hipLaunchKernelGGL(attend_split_kernel<3>, grid, block, lds, s, L, h0); break;
-      case 4: hipLaunchKernelGGL(attend_split_kernel<4>, grid, block, lds, s, L, h0); break;
-      case 5: hipLaunchKernelGGL(attend_split_kernel<5>, grid, block, lds, s, L, h0); break;
-      case 6: hipLaunchKernelGGL(attend_split_kernel<6>, grid, block, lds, s, L, h0); break;
-      case 7: hipLaunchKernelGGL(attend_split_kernel<7>, grid, block, lds, s, L, h0); break;
-      default: hipLaunchKernelGGL(attend_split_kernel<8>, grid, block, lds, s, L, h0); break;
+#define EBD_SPLIT(N)                                                                              \
+  case N:                                                                                         \
+    if (coop)                                                                                     \
+      hipLaunchKernelGGL((attend_split_kernel<N, true>), grid, block, lds, s, L, h0);             \
+    else                                                                                          \
+      hipLaunchKernelGGL((attend_split_kernel<N, false>), grid, block, lds, s, L, h0);            \
+    break;
+#define EBD_SPLIT_SOLO(N)                                                                         \
+  case N:                                                                                         \
+    hipLaunchKernelGGL((attend_split_kernel<N, false>), grid, block, lds, s, L, h0);              \
+    break;
+      EBD_SPLIT(1)
+      EBD_SPLIT(2)
+      EBD_SPLIT(3)
+      EBD_SPLIT(4)
+      EBD_SPLIT_SOLO(5)
+      EBD_SPLIT_SOLO(6)
+      EBD_SPLIT_SOLO(7)
+      default: EBD_SPLIT_SOLO(8)
+#undef EBD_SPLIT
+#undef EBD_SPLIT_SOLO
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -209,6 +209,13 @@ ebd_status attend_launch(const ebd_attend_params *p, const uint16_t *q, const ui
   L.U = p->num_units;
   L.G = p->group;
   L.nsplit = nsplit;
+  // a unit of 2..4 splits runs them as one work-group's waves, the last of which finalizes
+  // (up to kCoopMaxHeads query heads: with more, that kernel variant would exceed its registers)
+  L.wpg = (nsplit > 1 && nsplit <= kCoopMaxSplits && p->group <= kCoopMaxHeads &&
+           (size_t)nsplit * attend_part_lds_bytes(sr, p->group) <= kCoopLdsMax)
+              ? nsplit
+              : 1;
+  L.coop_counter = 0;
   L.split_rows = sr;
   L.nchunk = attend_chunks(sr);
   L.rec = attend_record_floats(sr);
@@ -240,7 +247,7 @@ ebd_status attend_launch(const ebd_attend_params *p, const uint16_t *q, const ui
     const hipError_t e1 = timing ? timed("attend_split", s, [&] { return launch_attend_split(L, s); })
                                  : launch_attend_split(L, s);
     if (e1 != hipSuccess) return EBD_ERR_HIP;
-    if (L.nsplit > 1) {
+    if (L.nsplit > 1 && L.wpg == 1) {
       const hipError_t e2 =
           timing ? timed("attend_finalize", s, [&] { return launch_attend_finalize(L, s); })
                  : launch_attend_finalize(L, s);

@@ -31,6 +31,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
                                            kRsrcWord3);
 }
 
+// Ordering of LDS and global memory between the lanes of one wave: what __syncthreads gives a
+// one-wave work-group (every prior access of the wave complete, no compiler motion across it),
+// without the work-group barrier.  Code that one wave of a larger work-group runs alone (the
+// attention finalize) synchronises with this.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 // bf16 halves of a 32-bit word -> fp32 (exact).
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }

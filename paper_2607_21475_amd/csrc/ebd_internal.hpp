@@ -23,6 +23,9 @@ constexpr int kSplitMinRows = 256;   // default split length floor
 constexpr int kSplitWaves = 1536;    // default: cut units until the launch has this many waves
 constexpr int kSplitRowsLimit = 8192;  // largest split a caller may ask for (LDS of one wave)
 constexpr int kMaxSplits = 4096;       // splits per unit (the finalize keeps a scale per split and head in LDS)
+constexpr int kCoopMaxSplits = 4;      // units of 2..4 splits run them as the waves of one work-group
+constexpr int kCoopMaxHeads = 4;       // ... when the unit has at most this many query heads
+constexpr size_t kCoopLdsMax = 61440;  // ... and their LDS stays within 60 KB per work-group
 constexpr size_t kSplitLdsBudget = 20480;  // LDS of one split wave at two waves per SIMD (160 KB / 8)
 constexpr int kResidentWaves = 2048;       // attention waves resident at once: two per SIMD, 256 CUs
 constexpr int kScoresMaxQueries = 64;  // queries per ebd_scores call (four MFMA blocks)
@@ -85,6 +88,8 @@ struct EvictLaunch {
 
 struct AttendLaunch {
   int32_t U, G, nsplit, split_rows, nhb;
+  int32_t wpg;           // waves per work-group: 1, or nsplit (a unit's splits in one work-group)
+  int32_t coop_counter;  // float offset in LDS of the arrival count (wpg > 1; set per head block)
   int32_t nchunk, rec;  // chunks per split, floats per record
   int32_t plain;        // 1: the uncorrected pass (no offset; writes y and lse only)
   const int64_t *cap_off;

@@ -323,6 +323,12 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([8192] * 3, 4, 0.5, 2048),                # four chunks per split, the last one likewise
     ([6144] * 2, 2, 0.7, 64),                  # > 64 splits: split scalars combined in batches
     ([16384] * 2, 4, 0.5, 64),                 # 128 splits: candidate blocks read from the records
+    # 2..4 splits and <= 4 heads: a unit's splits are the waves of one work-group, the last to
+    # arrive finalizes (ragged units whose later splits are empty, an empty unit)
+    ([2048, 777, 100, 5, 0, 3000], 4, 0.5, 512),
+    ([16384] * 3, 4, 0.25, 2048),              # three splits
+    ([6144] * 4, 1, 0.5, 1024),                # four splits, G = 1
+    ([3000, 1500, 2900], 3, 0.6, 1024),        # two splits, G = 3
 ])
 def test_attend_parity(lengths, G, budget, split):
     _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))
@@ -338,6 +344,7 @@ def test_attend_parity(lengths, G, budget, split):
 @pytest.mark.parametrize("lengths,G,split", [
     ([6144] * 6, 7, 0),                       # fused finalize
     ([4096, 300, 0, 9000], 4, 256),           # several splits, an empty unit
+    ([4096, 300, 0, 9000], 4, 1024),          # the same in one work-group per unit (three splits)
 ])
 def test_attend_without_offset(lengths, G, split):
     """EBD_F_NO_OFFSET: the uncorrected retained softmax as output, the Hajek certificate."""
@@ -518,6 +525,8 @@ def _dominated_unit(rng, n, G, q, boost, pi_floor=1e-6, tail_pi=(0.05, 1.0)):
     (4, 1500, 9.0, 0, False),    # 1e5 to 1e7-fold: the floor row alone makes yhat to fp32 precision
     (4, 1500, 4.0, 0, True),     # two identical dominating rows: the direct re-summation
     (7, 3000, 3.0, 512, True),
+    (4, 1500, 4.0, 512, False),  # three splits in one work-group: pivots meet in its finalize
+    (2, 1500, 9.0, 768, True),   # two splits in one work-group, direct re-summation
 ])
 def test_attend_vhat_dominant_tail_row(G, n, boost, split, dup):
     """A floor row (pi = 1e-6) retained and dominating Nhat: yhat ~ v_j, so the one-pass

@@ -27,7 +27,7 @@ def _both(lengths, G, budget, split, seed):
     ref = cache.attend_certify(out, q, split_rows=split)
     p = ebd.attend_params(U, G, out.max_cap, out.cap_off, split)
     need = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, p)
-    assert not cache.fused_finalize(need, U, G)  # split records are used
+    assert cache.uses_split_records(need, U, G)
     assert need <= ebd.EBD_NOALLOC_SCRATCH_BYTES
     got = {k: torch.full(ref[k].shape, float("nan"), dtype=torch.float32, device="cuda")
            for k in ("y", "vhat", "lse", "b", "r")}
