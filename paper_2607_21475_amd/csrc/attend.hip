@@ -1105,7 +1105,7 @@ __global__ __launch_bounds__(COOP ? 64 * kCoopMaxSplits : 64, 2) void attend_spl
   constexpr bool coop = COOP;
   const int sp = coop ? wave : bid % L.nsplit;
   const int u = coop ? bid : bid / L.nsplit;
-  const int lane = threadIdx.x & 63;
+  const int lane = (int)__lane_id();  // recomputed where needed rather than kept live (registers)
   const int g = lane >> 4, c = lane & 15;
   // this wave's LDS: [nchunk][GB][kChunkFloats] chunk blocks, then [GB][kPivFloats] pivot lists
   float *s_chunk = s_lds + (coop ? (size_t)wave * (L.nchunk * kChunkFloats + kPivFloats) * GB : 0);
@@ -1477,7 +1477,6 @@ hipError_t launch_attend_split(const AttendLaunch &L0, hipStream_t s) {
     L.coop_counter = L.wpg > 1 ? attend_coop_counter(L, gb) : 0;
     const size_t lds = attend_split_lds(L, gb);
     const bool coop = L.wpg > 1;
-    if (coop && gb > kCoopMaxHeads) return hipErrorInvalidValue;
     switch (gb) {
 #define EBD_SPLIT(N)                                                                              \
   case N:                                                                                         \
@@ -1486,20 +1485,15 @@ hipError_t launch_attend_split(const AttendLaunch &L0, hipStream_t s) {
     else                                                                                          \
       hipLaunchKernelGGL((attend_split_kernel<N, false>), grid, block, lds, s, L, h0);            \
     break;
-#define EBD_SPLIT_SOLO(N)                                                                         \
-  case N:                                                                                         \
-    hipLaunchKernelGGL((attend_split_kernel<N, false>), grid, block, lds, s, L, h0);              \
-    break;
       EBD_SPLIT(1)
       EBD_SPLIT(2)
       EBD_SPLIT(3)
       EBD_SPLIT(4)
-      EBD_SPLIT_SOLO(5)
-      EBD_SPLIT_SOLO(6)
-      EBD_SPLIT_SOLO(7)
-      default: EBD_SPLIT_SOLO(8)
+      EBD_SPLIT(5)
+      EBD_SPLIT(6)
+      EBD_SPLIT(7)
+      default: EBD_SPLIT(8)
 #undef EBD_SPLIT
-#undef EBD_SPLIT_SOLO
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -210,9 +210,8 @@ ebd_status attend_launch(const ebd_attend_params *p, const uint16_t *q, const ui
   L.G = p->group;
   L.nsplit = nsplit;
   // a unit of 2..4 splits runs them as one work-group's waves, the last of which finalizes
-  // (up to kCoopMaxHeads query heads: with more, that kernel variant would exceed its registers)
-  L.wpg = (nsplit > 1 && nsplit <= kCoopMaxSplits && p->group <= kCoopMaxHeads &&
-           (size_t)nsplit * attend_part_lds_bytes(sr, p->group) <= kCoopLdsMax)
+  L.wpg = (nsplit > 1 && nsplit <= kCoopMaxSplits &&
+           (size_t)nsplit * attend_part_lds_bytes(sr, std::min(p->group, kHeadBlock)) <= kCoopLdsMax)
               ? nsplit
               : 1;
   L.coop_counter = 0;

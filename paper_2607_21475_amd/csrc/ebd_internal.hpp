@@ -24,7 +24,6 @@ constexpr int kSplitWaves = 1536;    // default: cut units until the launch has 
 constexpr int kSplitRowsLimit = 8192;  // largest split a caller may ask for (LDS of one wave)
 constexpr int kMaxSplits = 4096;       // splits per unit (the finalize keeps a scale per split and head in LDS)
 constexpr int kCoopMaxSplits = 4;      // units of 2..4 splits run them as the waves of one work-group
-constexpr int kCoopMaxHeads = 4;       // ... when the unit has at most this many query heads
 constexpr size_t kCoopLdsMax = 61440;  // ... and their LDS stays within 60 KB per work-group
 constexpr size_t kSplitLdsBudget = 20480;  // LDS of one split wave at two waves per SIMD (160 KB / 8)
 constexpr int kResidentWaves = 2048;       // attention waves resident at once: two per SIMD, 256 CUs

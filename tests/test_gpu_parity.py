@@ -329,6 +329,9 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([16384] * 3, 4, 0.25, 2048),              # three splits
     ([6144] * 4, 1, 0.5, 1024),                # four splits, G = 1
     ([3000, 1500, 2900], 3, 0.6, 1024),        # two splits, G = 3
+    ([6144] * 4, 7, 0.25, 1024),               # two splits, G = 7
+    ([3000, 1500, 2900, 0], 8, 0.5, 512),      # four splits, G = 8, an empty unit
+    ([3000, 1500], 12, 0.4, 768),              # two head blocks (8 + 4), two splits each
 ])
 def test_attend_parity(lengths, G, budget, split):
     _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))
