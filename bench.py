@@ -67,13 +67,16 @@ def load_traffic(workload: str, kernel: str):
 
 
 def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str,
-                  out_dir: str = "") -> int:
+                  out_dir: str = "", req_dir: str = "") -> int:
     """Per-launch HBM bytes of the library's kernels from two rocprofv3 --pmc csv runs.
 
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same counter reads
     for the 1 GiB device copy that --copy-calibration runs (1 GiB read, 1 GiB written).  The
     1 GiB read-only sum it also runs gives a second FETCH_SIZE scale, reported beside the first:
     the two agree when the counter's scale does not depend on the access mix.
+    With req_dir (a third run counting the L2's memory read requests by size,
+    TCC_EA0_RDREQ_{32B,64B,128B}_sum and TCC_EA0_RDREQ_sum), the fetched bytes are also summed
+    directly, 32, 64 or 128 bytes per request, with no calibration; both are reported.
     Writes profiles/hbm_traffic_<workload>.json (read by the benchmark while the kernel sources
     are unchanged), or the same file under out_dir.
     """
@@ -111,6 +114,19 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str,
     gib_kib = float(1 << 20)
     fscale = gib_kib / statistics.median(fcal)  # true KiB per counted KiB
     wscale = gib_kib / statistics.median(wcal)
+    sized = {}  # per kernel: mean fetched bytes from the request counts, and the sized share
+    sized_calib = None
+    if req_dir:
+        per = {n: load(req_dir, "TCC_EA0_RDREQ_%s_sum" % n) for n in ("32B", "64B", "128B")}
+        tot = load(req_dir, "TCC_EA0_RDREQ_sum")
+        for k in tot[0]:
+            b = sum(w * statistics.mean(per[n][0].get(k, [0.0]))
+                    for n, w in (("32B", 32), ("64B", 64), ("128B", 128)))
+            cnt = sum(statistics.mean(per[n][0].get(k, [0.0])) for n in ("32B", "64B", "128B"))
+            sized[k] = (b, cnt / max(statistics.mean(tot[0][k]), 1.0))
+        if per["128B"][1]:
+            sized_calib = sum(w * statistics.median(per[n][1]) for n, w in
+                              (("32B", 32), ("64B", 64), ("128B", 128)) if per[n][1]) / (1 << 30)
     kernels = {}
     for k in sorted(set(fetch) | set(write)):
         fb = statistics.mean(fetch.get(k, [0.0])) * fscale * 1024
@@ -118,15 +134,46 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str,
         kernels[k] = {"fetch_bytes_per_launch": int(fb), "write_bytes_per_launch": int(wb),
                       "bytes_per_launch": int(fb + wb),
                       "launches_profiled": len(fetch.get(k, []))}
+        if k in sized:
+            kernels[k]["fetch_bytes_by_request_size"] = int(sized[k][0])
+            kernels[k]["sized_request_share"] = round(sized[k][1], 4)
     rec = {"workload": workload, "kernel_sources_hash": kernel_sources_hash(),
            "fetch_scale": fscale, "write_scale": wscale,
            "fetch_scale_read_only_sum": (gib_kib / statistics.median(frcal)) if frcal else None,
+           "calibration_copy_gib_by_request_size": sized_calib,
            "kernels": kernels, "command": command}
     out_dir = out_dir or os.path.join(ROOT, "profiles")
     os.makedirs(out_dir, exist_ok=True)
     path = os.path.join(out_dir, "hbm_traffic_%s.json" % workload)
     json.dump(rec, open(path, "w"), indent=1)
     print(json.dumps(rec, indent=1))
+    return 0
+
+
+def summarize_trace(trace_dir: str) -> int:
+    """Markdown table of the library's kernel durations from a rocprofv3 --kernel-trace csv run,
+    grouped by kernel and launch shape (work-groups x threads), so that the same kernel template
+    on different workloads is listed apart."""
+    import csv
+    import glob
+    import statistics
+
+    groups = {}
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            name = r["Kernel_Name"]
+            if "ebd::" not in name:
+                continue
+            name = name.split("(")[0].replace("void ", "")
+            wg = int(r["Workgroup_Size_X"])
+            key = (name, int(r["Grid_Size_X"]) // max(wg, 1), wg)
+            dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3  # ns -> us
+            groups.setdefault(key, []).append(dur)
+    print("| Kernel | Work-groups x threads | Calls | Average (us) | Min (us) | Max (us) |")
+    print("|---|---|---|---|---|---|")
+    for (name, nwg, wg), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        print("| `%s` | %d x %d | %d | %.1f | %.1f | %.1f |"
+              % (name, nwg, wg, len(d), statistics.mean(d), min(d), max(d)))
     return 0
 
 
@@ -162,6 +209,10 @@ def main() -> int:
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/hbm_traffic_<workload>.json from rocprofv3 --pmc csv runs")
     ap.add_argument("--pmc-command", default="", help="command recorded in the summary")
+    ap.add_argument("--summarize-trace", default="", metavar="TRACE_DIR",
+                    help="print the library's kernel durations from a rocprofv3 --kernel-trace run")
+    ap.add_argument("--pmc-requests", default="", metavar="REQ_DIR",
+                    help="with --summarize-pmc: a third counter run of the read requests by size")
     ap.add_argument("--compare-arms", action="store_true",
                     help="instead of timing: errors of the sampling designs against full attention")
     ap.add_argument("--compare-units", type=int, default=256)
@@ -178,9 +229,12 @@ def main() -> int:
                          "grid (8 KV heads per cell, G = 1, per-unit budgets and contexts)")
     args = ap.parse_args()
 
+    if args.summarize_trace:
+        return summarize_trace(args.summarize_trace)
     if args.summarize_pmc:
         return summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
-                             args.workload or args.legs.split(",")[0], args.pmc_command)
+                             args.workload or args.legs.split(",")[0], args.pmc_command,
+                             req_dir=args.pmc_requests)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -226,7 +280,6 @@ def main() -> int:
     calib = copy_calibration(torch, args.copy_calibration)
     h = headline
     h["roofline"]["measured_copy_gbs"] = calib["copy_gbs"]
-    h["roofline"]["measured_read_gbs"] = calib["read_gbs"]
     line = {
         "metric": METRIC,
         "value": h["value"],
