@@ -58,20 +58,22 @@ struct Tile {
   float p[4];  // pi of rows 16t + 4 g + j
 };
 
-// Tile t of a split (rows 16t .. 16t + 15 counted from the split's first row).
+// Tile t of a split (rows 16t .. 16t + 15 counted from the split's first row).  Every byte of the
+// retained rows is read once per step, so the loads are non-temporal (kLoadNT): streamed without
+// being kept in the caches, which on this GPU reads markedly faster than the default policy.
 __device__ __forceinline__ void load_tile(Tile &T, __amdgpu_buffer_rsrc_t rK, __amdgpu_buffer_rsrc_t rV,
                                           __amdgpu_buffer_rsrc_t rP, int t, int g, int c) {
   const uint32_t rk = (uint32_t)(16 * t + c);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
     T.k[kb] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                            rK, rk * 256u + (uint32_t)(64 * kb + 16 * g), 0, 0));
+                                            rK, rk * 256u + (uint32_t)(64 * kb + 16 * g), 0, kLoadNT));
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const uint32_t r = (uint32_t)(16 * t + 4 * g + j);
     T.v[j] = __builtin_bit_cast(u32x4,
-                                __builtin_amdgcn_raw_buffer_load_b128(rV, r * 256u + 16u * c, 0, 0));
-    T.p[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rP, r * 4u, 0, 0));
+                                __builtin_amdgcn_raw_buffer_load_b128(rV, r * 256u + 16u * c, 0, kLoadNT));
+    T.p[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rP, r * 4u, 0, kLoadNT));
   }
 }
 

@@ -25,6 +25,8 @@ __device__ __forceinline__ float fast_sqrt(float x) { return __builtin_amdgcn_sq
 // the range return zeros and stores there are dropped, without touching memory, so tail tiles
 // and prefetches past a range need no clamping.
 constexpr int kRsrcWord3 = 0x00020000;  // 32-bit data format, untyped access
+// Cache-policy operand of the raw buffer loads: the non-temporal hint (nt), for data read once.
+constexpr int kLoadNT = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t nbytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)nbytes,
