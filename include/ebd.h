@@ -184,15 +184,19 @@ typedef struct ebd_attend_params {
  *            EBD_ST_BAD_LAYOUT when the unit holds more rows than max_rows (the rows past
  *            max_rows are not seen); 0 otherwise.  The outputs then cover the rows seen.
  *   vhat is accumulated in the same pass as C2 - 2 yhat.Cv + |yhat|^2 C0 (C0 = sum c,
- *   Cv = sum c v, C2 = sum c |v|^2, c = (1 - pi) (a/pi)^2); a head where these terms cancel
- *   (one tail row dominating both yhat and the variance) is summed again directly over the
- *   unit's rows, sum c |v - yhat|^2, in the same call.
+ *   Cv = sum c v, C2 = sum c |v|^2, c = (1 - pi) (a/pi)^2), with each head's largest-weight
+ *   row kept out of these sums and added back in closed form, so that one tail row dominating
+ *   both yhat and the variance does not make them cancel; a head where the other rows still
+ *   cancel (several identical dominating rows) is summed again directly over the unit's rows,
+ *   sum c |v - yhat|^2, in the same call.
  *   workspace: at least ebd_workspace_size(EBD_WS_ATTEND, p) bytes, 256-byte aligned; y must
  *   be 16-byte aligned.  After the call the workspace starts with two uint32 counts per (unit,
  *   block of 8 query heads): the 512-row chunks re-read to make the range term exact (0 when
  *   the kept candidates already decide it), then the heads whose vhat was summed directly.
- *   When every unit fits one split, the whole step is one kernel and the workspace holds only
- *   these counts.
+ *   Then, when units span several splits, one partial record per (unit, split, query head).
+ *   A unit of up to 4 splits runs them as the waves of one work-group, the last of which
+ *   finalizes it, so the step is one kernel; units of more splits take a second kernel that
+ *   combines the records.  When every unit fits one split the workspace holds only the counts.
  */
 ebd_status ebd_attend_certify(const ebd_attend_params *p, const uint16_t *q, const uint16_t *Kc,
                               const uint16_t *Vc, const float *pic, const int32_t *count,
