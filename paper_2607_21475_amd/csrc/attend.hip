@@ -26,9 +26,12 @@
 //   g^2 |v|^2 (g^2 = (1 - pi) w^2) plus the maxima of g |v| and of g over what it dropped, so
 //   a chunk holds 32 candidates per head with bounds for the rest.
 //   The running max m moves lazily (only by jumps of more than 2^8 in weight).
+//   A unit cut into 2..4 splits (when their LDS fits one work-group) runs them as the waves
+//   of one work-group instead of as separate work-groups.
 // Finalize (yhat, Vhat, ln Nhat, the exact range term b and the radius r): a unit that is one
-//   split is finalized by the same wave from LDS; a unit cut into several splits by
-//   attend_finalize (one wave per (unit, head block)), which combines the split records by
+//   split is finalized by the same wave from LDS; a unit whose splits share a work-group by the
+//   wave that arrives last (an LDS counter, work-group fences); any other unit cut into splits
+//   by attend_finalize (one wave per (unit, head block)).  The split records are combined by
 //   log-sum-exp.  Candidates are bounded a chunk block at a time; only those whose bound can
 //   still win are re-read, and a chunk is rescanned only if its non-candidate bound cannot
 //   exclude a larger term.  Where C2 - 2 yhat.Cv + |yhat|^2 C0 has cancelled (one tail row

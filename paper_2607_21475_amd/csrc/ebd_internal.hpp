@@ -16,7 +16,7 @@ constexpr int kSelectRegThreads = 128;       // evict_select_reg: two waves per 
 constexpr int kCopyThreads = 256;            // evict_copy: 16 lanes per 256-byte row
 constexpr int kCopyRows = 128;               // retained rows per evict_copy work-group
 
-constexpr int kAttendThreads = 64;   // one wave per (unit, split, head block)
+constexpr int kAttendThreads = 64;   // one wave per (unit, split, head block); wpg waves per work-group
 constexpr int kHeadBlock = 8;        // query heads handled together (MFMA rows: 8 weight + 8 variance)
 constexpr int kSplitMaxRows = 4096;  // default split length cap (bounds the launch's tail)
 constexpr int kSplitMinRows = 256;   // default split length floor
