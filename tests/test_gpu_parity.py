@@ -326,6 +326,8 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     # 2..4 splits and <= 4 heads: a unit's splits are the waves of one work-group, the last to
     # arrive finalizes (ragged units whose later splits are empty, an empty unit)
     ([2048, 777, 100, 5, 0, 3000], 4, 0.5, 512),
+    ([20000, 9000, 4100, 513, 0], 4, 0.6, 3072),  # four splits of six chunks, ragged units
+    ([9000, 7000, 300], 8, 0.5, 1536),         # three splits, G = 8
     ([16384] * 3, 4, 0.25, 2048),              # three splits
     ([6144] * 4, 1, 0.5, 1024),                # four splits, G = 1
     ([3000, 1500, 2900], 3, 0.6, 1024),        # two splits, G = 3
