@@ -76,8 +76,15 @@ __device__ __forceinline__ void load_tile(Tile &T, __amdgpu_buffer_rsrc_t rK, __
     const uint32_t r = (uint32_t)(16 * t + 4 * g + j);
     T.v[j] = __builtin_bit_cast(u32x4,
                                 __builtin_amdgcn_raw_buffer_load_b128(rV, r * 256u + 16u * c, 0, kLoadNT));
-    T.p[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rP, r * 4u, 0, kLoadNT));
   }
+  // pi of the row group's 4 consecutive rows in one 16-byte load (the range check is per dword:
+  // rows past the split read as zero, those before it are loaded)
+  const u32x4 pw = __builtin_bit_cast(
+      u32x4, __builtin_amdgcn_raw_buffer_load_b128(rP, (uint32_t)(16 * t + 4 * g) * 4u, 0, kLoadNT));
+  T.p[0] = __uint_as_float(pw.x);
+  T.p[1] = __uint_as_float(pw.y);
+  T.p[2] = __uint_as_float(pw.z);
+  T.p[3] = __uint_as_float(pw.w);
 }
 
 struct SplitState {
