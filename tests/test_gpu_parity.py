@@ -318,6 +318,9 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([16384] * 4, 4, 0.25, 0),                 # GQA 4, long cache
     ([2048, 777, 100, 5, 9000, 3000], 8, 0.3, 128),  # ragged tails, G = 8
     ([3000, 1500], 12, 0.2, 0),                # two head blocks (8 + 4)
+    ([4096, 1000], 32, 0.25, 0),               # four head blocks of 8
+    ([30000], 2, 0.245, 8192),                 # one split of the largest length (capacity 8064),
+                                               # finalized in place
     ([4096, 300], 9, 0.5, 256),                # 8 + 1
     ([6144] * 6, 7, 0.5, 512),                 # a candidate chunk ends on the loop's last tiles
     ([8192] * 3, 4, 0.5, 2048),                # four chunks per split, the last one likewise
