@@ -192,6 +192,17 @@ struct PieceEdges {
   }
 };
 
+// Streamed units (scores re-read from memory on every pass) start the iteration from a lambda
+// solved on a histogram of their positive tail scores, gathered in the statistics pass: the bins
+// are the fp32 bit patterns shifted right by kHistShift (the exponent and five mantissa bits, 32
+// bins per octave over every positive float; 64 KB of LDS, which these units do not use for
+// scores), each bin's scores taken at the bin's midpoint.  Started there, the iteration needs
+// fewer passes over the scores than from the literal m / sum s (a CPU replay on Pareto scores:
+// 2.0 instead of 3.6); the lambda it ends on is the same exact solve of the piece it finds.
+// (Staged units gain nothing from it: their passes read LDS.)
+constexpr int kHistShift = 18;
+constexpr int kHistBins = 1 << (31 - kHistShift);
+
 // The iteration for an interior lambda within the bracket [lo, hi] (g(lo) < m <= g(hi)),
 // starting at cur.  pass(lf, H, L, S, edges) evaluates the piece at lf.  A Newton step that
 // stays on the evaluated piece is final: the next pass would find the same piece and stop there,
@@ -362,6 +373,99 @@ __device__ __forceinline__ void gather_rows(const EvictLaunch &L, int64_t base, 
   }
 }
 
+// The start of a streamed unit's lambda iteration from its score histogram (every thread of the
+// NT-thread work-group calls it; the histogram's counts are complete in hc).  hc becomes the
+// counts' exclusive prefix and hm that of count x bin midpoint.  With the scores of every bin at
+// its midpoint, g(lambda) = H + eps L + lambda S is evaluated at each bin's breakpoint 1 / mid
+// (the bin and those above it clip at 1; the bins at or below eps / lambda, and the zero scores,
+// clip at eps); g falls as the bin rises, and the piece just below the highest bin whose
+// breakpoint still has g >= m is solved for lambda.  Returns `fallback` when no bin qualifies.
+template <int NT>
+__device__ __forceinline__ double hist_start(int *hc, float *hm, int *s_wc, float *s_ww, int &s_bin,
+                                             double m, float eps, double n_zero, double fallback) {
+  constexpr int NW = NT / 64;
+  constexpr int PER = kHistBins / NT;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  auto mid = [](int b) { return __uint_as_float(((uint32_t)b << kHistShift) | (1u << (kHistShift - 1))); };
+  __syncthreads();  // the counts are complete
+  int ct = 0;
+  float wt = 0.0f;  // the start is approximate: fp32 sums of count x midpoint suffice
+  for (int i = 0; i < PER; ++i) {
+    const int c = hc[PER * t + i];
+    ct += c;
+    wt = fmaf((float)c, mid(PER * t + i), wt);
+  }
+  // exclusive prefix of (ct, wt) over the threads: within the wave, then over the waves
+  int ic = ct;
+  float iw = wt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int xc = __shfl_up(ic, o);
+    const float xw = __shfl_up(iw, o);
+    if (lane >= o) {
+      ic += xc;
+      iw += xw;
+    }
+  }
+  if (lane == 63) {
+    s_wc[wv] = ic;
+    s_ww[wv] = iw;
+  }
+  __syncthreads();
+  int pc = 0, nc = 0;
+  float pw = 0.0f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if (w < wv) {
+      pc += s_wc[w];
+      pw += s_ww[w];
+    }
+    nc += s_wc[w];
+  }
+  pc += ic - ct;
+  pw += iw - wt;
+  if (t == 0) s_bin = -1;
+  for (int i = 0; i < PER; ++i) {  // in place: this thread's bins only
+    const int b = PER * t + i, c = hc[b];
+    hc[b] = pc;
+    hm[b] = pw;
+    pc += c;
+    pw = fmaf((float)c, mid(b), pw);
+  }
+  __syncthreads();  // the prefixes of every bin are in place
+  const double N = (double)nc;
+  auto count = [&](int b) { return (b + 1 < kHistBins ? hc[b + 1] : nc) - hc[b]; };
+  // g at the breakpoint of bin b (lambda_b = 1 / mid_b): H = bins >= b, L = bins below the bin
+  // of eps mid_b (and the zero scores), S = the bins between
+  auto piece = [&](int b, double &H, double &Lo, double &S) {
+    const int be = (int)(__float_as_uint(eps * mid(b)) >> kHistShift);
+    H = N - (double)hc[b];
+    Lo = (double)hc[be] + n_zero;
+    S = (double)hm[b] - (double)hm[be];
+  };
+  int best = -1;
+  for (int i = 0; i < PER; ++i) {
+    const int b = PER * t + i;
+    if (count(b) == 0) continue;
+    double H, Lo, S;
+    piece(b, H, Lo, S);
+    if (H + (double)eps * Lo + S / (double)mid(b) >= m) best = b;  // bins ascend: the last that qualifies
+  }
+  if (best >= 0) atomicMax(&s_bin, best);
+  __syncthreads();
+  const int b = s_bin;
+  if (b < 0) return fallback;
+  // just below the breakpoint the bin itself leaves H for the middle
+  double H, Lo, S;
+  piece(b, H, Lo, S);
+  const int cb = count(b);
+  H -= (double)cb;
+  S += (double)cb * (double)mid(b);
+  const double top = 1.0 / (double)mid(b);
+  const double lam = S > 0.0 ? (m - H - (double)eps * Lo) / S : top;
+  return (lam > 0.0 && lam <= top) ? lam : top;
+}
+
 template <int NT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4)))
 void evict_select_kernel(EvictLaunch L) {
@@ -371,6 +475,9 @@ void evict_select_kernel(EvictLaunch L) {
   __shared__ int s_tot[2][NT / 64];
   __shared__ int s_hist[256];
   __shared__ int s_sel[2];
+  __shared__ int s_hc[NT / 64];     // streamed units: per-wave histogram totals (counts, ...
+  __shared__ float s_hw[NT / 64];   // ... and count x midpoint) for the histogram's prefix
+  __shared__ int s_hb;              // the histogram bin where g crosses m
   int rbuf = 0;
   const int u = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -427,6 +534,16 @@ void evict_select_kernel(EvictLaunch L) {
     return tail4(gi, load_raw(gi), dummy);
   };
 
+  // Streamed units: LDS holds the histogram of the positive tail scores (counts, later their
+  // exclusive prefix) and the prefix of count x bin midpoint.
+  const bool hist = !staged && L.design != EBD_DESIGN_TOPK;
+  int *s_hcnt = reinterpret_cast<int *>(s_sc);
+  float *s_hmid = s_sc + kHistBins;
+  if (hist) {
+    for (int b = t; b < kHistBins; b += NT) s_hcnt[b] = 0;
+    __syncthreads();
+  }
+
   // Pass 0: read (and stage) the scores; tail statistics; bad-score flag.  Four groups per
   // thread are loaded before any is used so their latencies overlap.
   uint32_t bad = 0;
@@ -454,6 +571,7 @@ void evict_select_kernel(EvictLaunch L) {
         gsum += tail ? v[j] : 0.0f;
         s_minp = fminf(s_minp, pos ? v[j] : INFINITY);
         s_max = fmaxf(s_max, v[j]);
+        if (hist && pos) atomicAdd(&s_hcnt[__float_as_uint(v[j]) >> kHistShift], 1);
       }
       s_sum += (double)gsum;
       if (staged) reinterpret_cast<float4 *>(s_sc)[gi] = tv;
@@ -567,7 +685,9 @@ void evict_select_kernel(EvictLaunch L) {
   double lam = 0.0;
   if (!topk && !lambda_boundary(ts, m, eps, L.pi_mode, st, lam)) {
     const double lo0 = (double)eps / (double)s_max, hi0 = 1.0 / (double)s_minp;
-    lam = newton_lambda(m, eps, lo0, hi0, fmin(fmax(m / s_sum, lo0), hi0), newton_pass);
+    double start = m / s_sum;
+    if (hist) start = hist_start<NT>(s_hcnt, s_hmid, s_hc, s_hw, s_hb, m, eps, n_tail - n_pos, start);
+    lam = newton_lambda(m, eps, lo0, hi0, fmin(fmax(start, lo0), hi0), newton_pass);
   }
   const float lamf = (float)lam;
 
@@ -1197,7 +1317,8 @@ hipError_t launch_evict_select(const EvictLaunch &L, hipStream_t s) {
   if (evict_select_gathers(L)) {
     // eight waves per unit, two units per CU: scores staged in LDS (up to 64 KB per unit) or,
     // for longer units, streamed from memory on every pass
-    const size_t lds = (size_t)((L.stage_rows + 3) / 4) * 16;
+    const size_t lds = L.stage_rows > 0 ? (size_t)((L.stage_rows + 3) / 4) * 16
+                                         : (size_t)kHistBins * (sizeof(int) + sizeof(float));
     hipLaunchKernelGGL(evict_select_kernel<kSelectThreads>, grid, dim3(kSelectThreads), lds, s, L);
   } else if (g4 <= 2) hipLaunchKernelGGL(evict_select_reg_kernel<2>, grid, reg, 0, s, L);
   else if (g4 <= 4) hipLaunchKernelGGL(evict_select_reg_kernel<4>, grid, reg, 0, s, L);
