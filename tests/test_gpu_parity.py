@@ -651,6 +651,83 @@ def test_append_certain():
     assert _np(out.status)[0] & oracle.ST_CAP_OVERFLOW
 
 
+@pytest.mark.parametrize("lengths,G,split", [
+    ([3000, 2500, 4100, 700], 4, 0),     # one split per unit, finalized in place
+    ([3000, 2500, 4100, 700], 4, 1024),  # a unit's splits as the waves of one work-group
+    ([6144, 6144], 2, 256),              # split records, then the finalize launch
+])
+def test_decode_step_graph_replay(lengths, G, split):
+    """A decode step (append a pi = 1 row, then certified attention) captured in a HIP graph: the
+    library launches kernels only (no allocation, copy or memset), so the graph holds the whole
+    step.  Each replay, with eager work and a synchronization between replays, matches an eager
+    step on a twin cache bit for bit, and the last replay's outputs match the oracle."""
+    _say("graph replay of a decode step %s G=%d split=%d" % (lengths, G, split))
+    import paper_2607_21475_amd as ebd
+    from paper_2607_21475_amd import cache
+
+    U, steps = len(lengths), 4
+    K, V, seq_off, sc, _ = _inputs(lengths, seed=23, group=G)
+    cap_host = cache.plan_capacity(lengths, 0.25, 4, 64, extra=steps + 1)
+    A = cache.evict(K, V, sc, seq_off, lengths, budget_frac=0.25, seed=7, cap_off_host=cap_host)
+    B = cache.evict(K, V, sc, seq_off, lengths, budget_frac=0.25, seed=7, cap_off_host=cap_host)
+    p = ebd.attend_params(U, G, A.max_cap, A.cap_off, split)
+    need = ebd.ebd_workspace_size(ebd.EBD_WS_ATTEND, p)
+    wsA, wsB = ebd.workspace(need), ebd.workspace(need)
+    keys = ("y", "vhat", "lse", "b", "r", "st")
+
+    def outputs():
+        o = {k: torch.empty((U, G), dtype=torch.float32, device="cuda") for k in keys[1:5]}
+        o["y"] = torch.empty((U, G, 128), dtype=torch.float32, device="cuda")
+        o["st"] = torch.empty((U,), dtype=torch.int32, device="cuda")
+        return o
+
+    oA, oB = outputs(), outputs()
+    qs = [synth.make_queries(U, G, seed=40 + t, device="cuda") for t in range(steps + 1)]
+    kn = [synth.make_queries(U, 1, seed=50 + t, device="cuda")[:, 0].contiguous() for t in range(steps + 1)]
+    vn = [synth.make_queries(U, 1, seed=60 + t, device="cuda")[:, 0].contiguous() for t in range(steps + 1)]
+    pos = [torch.tensor([n + t for n in lengths], dtype=torch.int32, device="cuda")
+           for t in range(steps + 1)]
+    q_s, k_s, v_s, p_s = qs[0].clone(), kn[0].clone(), vn[0].clone(), pos[0].clone()
+
+    def step(rc, o, ws, q, k, v, ps):
+        ebd.ebd_append_certain(U, rc.cap_off, rc.count, k, v, rc.Kc, rc.Vc, rc.pic, rc.idxc, ps,
+                               rc.status)
+        ebd.ebd_attend_certify(p, q, rc.Kc, rc.Vc, rc.pic, rc.count, o["y"], o["vhat"], o["lse"], ws,
+                               brange=o["b"], radius=o["r"], status=o["st"])
+
+    # step 0 eagerly on both caches (the twin's on a side stream, as before a capture), then capture
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(B, oB, wsB, q_s, k_s, v_s, p_s)
+    torch.cuda.current_stream().wait_stream(side)
+    step(A, oA, wsA, qs[0], kn[0], vn[0], pos[0])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(B, oB, wsB, q_s, k_s, v_s, p_s)
+    torch.cuda.synchronize()
+    for t in range(1, steps + 1):
+        q_s.copy_(qs[t])
+        k_s.copy_(kn[t])
+        v_s.copy_(vn[t])
+        p_s.copy_(pos[t])
+        g.replay()
+        step(A, oA, wsA, qs[t], kn[t], vn[t], pos[t])
+        torch.cuda.synchronize()
+        for k in keys:
+            assert torch.equal(oA[k], oB[k]), (t, k)
+        assert torch.equal(A.count, B.count), t
+        coff, cnt = _np(A.cap_off), _np(A.count)
+        for k in ("Kc", "Vc", "pic", "idxc"):  # the retained rows (capacity past them is unwritten)
+            a, b = getattr(A, k), getattr(B, k)
+            for u in range(U):
+                lo, hi = int(coff[u]), int(coff[u] + cnt[u])
+                assert torch.equal(a[lo:hi], b[lo:hi]), (t, k, u)
+    assert not _np(oB["st"]).any()
+    np.testing.assert_array_equal(_np(B.count), _np(A.count))
+    _check_attend(B, oB, q_s, G)
+
+
 # ------------------------------------------------------------------------------------------
 # Full-size workload (the benchmark's launch configuration), sampled units
 # ------------------------------------------------------------------------------------------
