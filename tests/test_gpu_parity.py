@@ -337,6 +337,11 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([6144] * 4, 7, 0.25, 1024),               # two splits, G = 7
     ([3000, 1500, 2900, 0], 8, 0.5, 512),      # four splits, G = 8, an empty unit
     ([3000, 1500], 12, 0.4, 768),              # two head blocks (8 + 4), two splits each
+    ([2048, 777, 100, 5, 3000], 5, 0.3, 0),    # G = 5, one split per unit
+    ([6144] * 3, 6, 0.25, 1024),               # G = 6, two splits in one work-group
+    ([4096] * 2, 5, 0.5, 256),                 # G = 5, split records and the finalize launch
+    ([3000, 2000], 10, 0.4, 0),                # head blocks of 8 + 2
+    ([2500] * 2, 16, 0.3, 512),                # two full head blocks, two splits each
 ])
 def test_attend_parity(lengths, G, budget, split):
     _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))
