@@ -113,6 +113,7 @@ def _check_evict(lengths, K, V, seq_off, sc, out, n_sink=4, n_recent=64, budget=
     ([0, 1, 5, 70, 100, 777, 2047, 2048, 2049, 4096, 5000, 6144], 0.2),
     ([1, 3, 511, 512, 513, 1024], 0.3),
     ([2000, 17, 1500], 0.15),
+    ([3000, 4096, 2500, 100, 2049], 0.3),     # 8 groups per thread
 ])
 def test_evict_parity(lengths, budget):
     _say("evict parity lengths=%s budget=%s" % (lengths[:6], budget))
