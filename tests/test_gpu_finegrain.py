@@ -37,6 +37,11 @@ def _np(t):
     ([4096] * 6, 7, 0.25, 64),
     ([6144, 0, 300, 9000], 4, 0.1, 64),
     ([3000, 1500], 12, 0.3, 128),          # two head blocks, added in order
+    ([3000, 700], 1, 0.3, 64),             # G = 1, 2, 3, 5, 6
+    ([2048, 2048], 2, 0.25, 64),
+    ([1500, 2500], 3, 0.3, 128),
+    ([2000, 40], 5, 0.25, 64),
+    ([2500, 900], 6, 0.3, 64),
 ])
 def test_block_contributions(lengths, G, budget, block_rows):
     _say("block contributions lengths=%s G=%d" % (lengths, G))

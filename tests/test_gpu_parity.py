@@ -343,6 +343,9 @@ def _check_attend(out, res, q, G, tol_y=2e-3, tol_c=1e-2):
     ([4096] * 2, 5, 0.5, 256),                 # G = 5, split records and the finalize launch
     ([3000, 2000], 10, 0.4, 0),                # head blocks of 8 + 2
     ([2500] * 2, 16, 0.3, 512),                # two full head blocks, two splits each
+    ([2048, 3000, 700], 6, 0.3, 0),            # G = 6, one split per unit
+    ([6144] * 2, 3, 0.5, 256),                 # G = 3 and G = 6, split records and the finalize
+    ([4096] * 2, 6, 0.4, 256),                 # launch
 ])
 def test_attend_parity(lengths, G, budget, split):
     _say("attend parity lengths=%s G=%d budget=%s split=%d" % (lengths[:4], G, budget, split))

@@ -90,14 +90,16 @@ def test_scores_causal_prefill_queries():
     _check(K, q, seq_off, s, qpos=qpos)
 
 
-def test_scores_accumulate_over_calls():
-    """More than 64 queries: a second call adds its queries' mass to the first call's scores."""
+@pytest.mark.parametrize("extra", [32, 16, 40, 64])
+def test_scores_accumulate_over_calls(extra):
+    """More than 64 queries: a second call (1 to 4 blocks of 16 queries) adds its queries' mass to
+    the first call's scores."""
     from paper_2607_21475_amd import cache
 
     lengths = [4096, 1500]
-    _say("scores accumulate")
+    _say("scores accumulate, 64 + %d queries" % extra)
     K, _, seq_off = synth.make_cache(lengths, seed=6, device="cuda")
-    q = synth.make_queries(len(lengths), 96, seed=7, device="cuda")
+    q = synth.make_queries(len(lengths), 64 + extra, seed=7, device="cuda")
     s, ws = cache.importance_scores(K, seq_off, q[:, :64].contiguous(), max(lengths))
     s, _ = cache.importance_scores(K, seq_off, q[:, 64:].contiguous(), max(lengths), scores=s,
                                    accumulate=True, ws=ws)
