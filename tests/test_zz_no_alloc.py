@@ -1,7 +1,8 @@
 """The attention entry point without allocation (ebd_attend_certify_noalloc), through the C ABI,
 against the workspace entry point ebd_attend_certify on the same inputs: two calls in a row, the
 second on a smaller input, both with units cut into several splits so that the split records
-live in the library's scratch array."""
+live in the library's scratch array; then a third whose units' two splits run as the waves of one
+work-group (combined in LDS: of the scratch array only the per-unit diagnostic words are used)."""
 import numpy as np
 import pytest
 import torch
@@ -59,6 +60,8 @@ def test_noalloc_matches_workspace_entry_point_twice():
     _check(*_both([6144] * 40, 4, 0.25, 512, seed=61))
     _say("no-alloc call 2 (smaller): 9 units x 3000, G = 7, 10%, 256-row splits")
     _check(*_both([3000] * 9, 7, 0.10, 256, seed=62))
+    _say("no-alloc call 3: 12 units x 4000, G = 4, 30%, two splits as the waves of one work-group")
+    _check(*_both([4000] * 12, 4, 0.30, 1024, seed=63))
 
 
 def test_noalloc_rejects_launches_beyond_its_scratch():
